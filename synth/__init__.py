@@ -1,0 +1,17 @@
+"""Seeded synthetic inputs shared by the CPU oracle and the GPU path.
+
+This package holds the workload shapes and the random-number recipe only; it
+contains none of the DiT block's arithmetic.  Both sides of every parity check
+read the exact same stored bits from here.
+"""
+from .workloads import Workload, WORKLOADS, get_workload
+from .gen import (
+    bf16_bits, generate_block_inputs, generate_tensor, TensorSpec,
+    block_tensor_specs, generate_attention_inputs, generate_sampled_rows,
+)
+
+__all__ = [
+    "Workload", "WORKLOADS", "get_workload", "bf16_bits", "generate_block_inputs",
+    "generate_tensor", "TensorSpec", "block_tensor_specs",
+    "generate_attention_inputs", "generate_sampled_rows",
+]

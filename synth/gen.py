@@ -1,0 +1,187 @@
+"""Seeded generator for the block's inputs and weights.
+
+Recipe (one fixed draw per named tensor, independent of generation order):
+
+* every tensor has a stable id; its values are drawn with NumPy's PCG64 via
+  ``default_rng([13501, workload_id, tensor_id, chunk])`` in chunks of
+  ``CHUNK`` elements, so large tensors can be drawn on several threads and still
+  give the same bits;
+* standard normal draws in float32, scaled by the tensor's std and shifted by
+  its mean, then stored either as float32 or as bfloat16 bits obtained by
+  round-to-nearest-even on the float32 bit pattern;
+* latents and text embeddings ~ N(0, 1); Linear weights and biases
+  ~ N(0, 0.02^2); norm gains ~ 1 + N(0, 0.02^2); LayerNorm shift ~ N(0, 0.02^2);
+  timesteps ~ U[0, 1000) (float32).
+
+bfloat16 values travel as ``uint16`` arrays of their bit patterns.
+"""
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
+from typing import Dict, Iterable, Optional, Sequence, Tuple
+import os
+
+import numpy as np
+
+from .workloads import Workload
+
+SEED = 13501
+CHUNK = 1 << 22
+
+
+def bf16_bits(a: np.ndarray) -> np.ndarray:
+    """float32 array -> uint16 bfloat16 bit patterns, round to nearest even."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+@dataclass(frozen=True)
+class TensorSpec:
+    name: str
+    tid: int
+    shape: Tuple[int, ...]
+    dist: str           # "normal" or "uniform"
+    mean: float = 0.0
+    std: float = 1.0
+    lo: float = 0.0
+    hi: float = 1.0
+    dtype: Optional[str] = None   # None: the workload's dtype; "f32" forces float32
+
+
+def _fill(spec: TensorSpec, wid: int, threads: int, as_bf16: bool) -> np.ndarray:
+    n = int(np.prod(spec.shape)) if spec.shape else 1
+    out = np.empty(n, dtype=np.uint16 if as_bf16 else np.float32)
+    chunks = [(c, c * CHUNK, min(n, (c + 1) * CHUNK)) for c in range((n + CHUNK - 1) // CHUNK)]
+
+    def work(ch):
+        c, a, b = ch
+        rng = np.random.default_rng([SEED, wid, spec.tid, c])
+        if spec.dist == "normal":
+            v = rng.standard_normal(b - a, dtype=np.float32)
+            if spec.std != 1.0:
+                v *= np.float32(spec.std)
+            if spec.mean != 0.0:
+                v += np.float32(spec.mean)
+        elif spec.dist == "uniform":
+            v = rng.random(b - a, dtype=np.float32)
+            v = (v * np.float32(spec.hi - spec.lo) + np.float32(spec.lo)).astype(np.float32)
+            # guard the half-open interval against rounding up to hi
+            v = np.minimum(v, np.nextafter(np.float32(spec.hi), np.float32(spec.lo)))
+        else:
+            raise ValueError(spec.dist)
+        out[a:b] = bf16_bits(v) if as_bf16 else v
+
+    if len(chunks) > 1 and threads > 1:
+        with ThreadPoolExecutor(min(threads, len(chunks))) as ex:
+            list(ex.map(work, chunks))
+    else:
+        for ch in chunks:
+            work(ch)
+    return out.reshape(spec.shape)
+
+
+def generate_tensor(spec: TensorSpec, wl: Workload, threads: Optional[int] = None) -> np.ndarray:
+    threads = threads or min(16, os.cpu_count() or 1)
+    dt = spec.dtype or wl.dtype
+    if dt not in ("f32", "bf16"):
+        raise ValueError(dt)
+    return _fill(spec, wl.wid, threads, dt == "bf16")
+
+
+def block_tensor_specs(wl: Workload) -> Dict[str, TensorSpec]:
+    """All inputs and weights of one block, keyed by name ([out, in] weights)."""
+    D, F, Dff, d = wl.hidden, wl.freq_dim, wl.mlp_hidden, wl.head_dim
+    W = 0.02
+    specs = [
+        TensorSpec("x", 1, (wl.n_rows, D), "normal"),
+        TensorSpec("txt", 2, (wl.n_txt, D), "normal"),
+        TensorSpec("t", 3, (wl.n_req,), "uniform", lo=0.0, hi=1000.0, dtype="f32"),
+        TensorSpec("w_t1", 10, (D, F), "normal", std=W),
+        TensorSpec("b_t1", 11, (D,), "normal", std=W),
+        TensorSpec("w_t2", 12, (D, D), "normal", std=W),
+        TensorSpec("b_t2", 13, (D,), "normal", std=W),
+        TensorSpec("w_ada", 14, (6 * D, D), "normal", std=W),
+        TensorSpec("b_ada", 15, (6 * D,), "normal", std=W),
+        TensorSpec("w_qkv", 16, (3 * D, D), "normal", std=W),
+        TensorSpec("b_qkv", 17, (3 * D,), "normal", std=W),
+        TensorSpec("g_q", 18, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("g_k", 19, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("w_o", 20, (D, D), "normal", std=W),
+        TensorSpec("b_o", 21, (D,), "normal", std=W),
+        TensorSpec("g_ca", 22, (D,), "normal", mean=1.0, std=W),
+        TensorSpec("b_ca", 23, (D,), "normal", std=W),
+        TensorSpec("w_cq", 24, (D, D), "normal", std=W),
+        TensorSpec("b_cq", 25, (D,), "normal", std=W),
+        TensorSpec("w_ckv", 26, (2 * D, D), "normal", std=W),
+        TensorSpec("b_ckv", 27, (2 * D,), "normal", std=W),
+        TensorSpec("g_cq", 28, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("g_ck", 29, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("w_co", 30, (D, D), "normal", std=W),
+        TensorSpec("b_co", 31, (D,), "normal", std=W),
+        TensorSpec("w_up", 32, (Dff, D), "normal", std=W),
+        TensorSpec("b_up", 33, (Dff,), "normal", std=W),
+        TensorSpec("w_dn", 34, (D, Dff), "normal", std=W),
+        TensorSpec("b_dn", 35, (D,), "normal", std=W),
+    ]
+    return {s.name: s for s in specs}
+
+
+WEIGHT_NAMES = (
+    "w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada", "w_qkv", "b_qkv", "g_q", "g_k",
+    "w_o", "b_o", "g_ca", "b_ca", "w_cq", "b_cq", "w_ckv", "b_ckv", "g_cq", "g_ck",
+    "w_co", "b_co", "w_up", "b_up", "w_dn", "b_dn",
+)
+
+
+def generate_block_inputs(wl: Workload, names: Optional[Iterable[str]] = None,
+                          threads: Optional[int] = None) -> Dict[str, np.ndarray]:
+    specs = block_tensor_specs(wl)
+    names = list(names) if names is not None else list(specs)
+    return {n: generate_tensor(specs[n], wl, threads) for n in names}
+
+
+def generate_attention_inputs(wl: Workload, threads: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """Synthetic q, k, v ~ N(0, 1) for the self-attention stage on its own.
+
+    Shapes are [rows, heads, head_dim] over the lengths and heads the attention
+    stage sees (the full request lengths and the head share for an SP share).
+    Also an attention output ``o`` ~ N(0, 1) of shape [rows, D] for the
+    post-attention stage of an SP share, whose producer (the exchange of heads
+    for rows between GPUs) is not part of one GPU's work.
+    """
+    heads = wl.attn_heads or wl.n_heads
+    n_attn = wl.cu_attn()[-1]
+    specs = {
+        "q": TensorSpec("q", 40, (n_attn, heads, wl.head_dim), "normal"),
+        "k": TensorSpec("k", 41, (n_attn, heads, wl.head_dim), "normal"),
+        "v": TensorSpec("v", 42, (n_attn, heads, wl.head_dim), "normal"),
+        "o": TensorSpec("o", 43, (wl.n_rows, wl.hidden), "normal"),
+    }
+    return {n: generate_tensor(s, wl, threads) for n, s in specs.items()}
+
+
+def generate_sampled_rows(wl: Workload, n_per_req: int, sample_id: int = 0,
+                          attn: bool = False) -> np.ndarray:
+    """Sorted global row indices: a seeded sample of each request's rows that
+    always includes the first and last row and rows at frame boundaries."""
+    rng = np.random.default_rng([SEED, wl.wid, 1000 + sample_id])
+    cu = wl.cu_attn() if attn else wl.cu_seqlens()
+    out = []
+    for r in range(wl.n_req):
+        n = cu[r + 1] - cu[r]
+        Fg, Hg, Wg = wl.grids[r]
+        must = {0, n - 1}
+        frame = Hg * Wg
+        for f in range(1, Fg):
+            if f * frame < n:
+                must.add(f * frame - 1)
+                must.add(f * frame)
+        must = sorted(must)[: max(2, n_per_req // 2)]
+        k = max(0, min(n, n_per_req) - len(must))
+        pool = np.setdiff1d(np.arange(n), np.array(must))
+        pick = rng.choice(pool, size=min(k, len(pool)), replace=False) if k else np.array([], int)
+        rows = np.unique(np.concatenate([np.array(must, dtype=np.int64), pick.astype(np.int64)]))
+        out.append(rows + cu[r])
+    return np.concatenate(out)

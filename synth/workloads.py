@@ -1,0 +1,110 @@
+"""Workload shapes for one DiT block on one GPU's share of a request.
+
+The request classes follow the paper's evaluation workloads (section 6.1,
+Experimental Setup): Wan2.2 videos of 480x832 and 720x1280 pixels with 81
+frames, and Qwen-Image images of 1024x1024 and 1536x1536 pixels.  Token counts
+assume 4x temporal and 8x spatial VAE compression followed by 1x2x2 patches
+(2x2 for images); the paper states neither factor, so these counts are a
+consistent reading, not a quotation:
+
+* 480p video: latent 21x60x104 -> 21*30*52 = 32,760 tokens
+* 720p video: latent 21x90x160 -> 21*45*80 = 75,600 tokens
+* 1024^2 image: latent 128x128 -> 64*64 = 4,096 tokens
+* 1536^2 image: latent 192x192 -> 96*96 = 9,216 tokens
+
+Nothing here computes anything of the block; it is shared by the oracle and the
+GPU path as plain data.
+"""
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    wid: int                         # seed component, fixed per workload
+    dtype: str                       # "f32" or "bf16": storage and GEMM operand type
+    hidden: int                      # D
+    n_heads: int                     # H for the per-token stages (H*d == D)
+    head_dim: int                    # d
+    mlp_hidden: int                  # Dff
+    freq_dim: int                    # F, width of the sinusoidal timestep encoding
+    rope_sections: Tuple[int, int, int]   # (d_t, d_h, d_w); (0,0,0) disables rotary
+    grids: Tuple[Tuple[int, int, int], ...]  # full (F, H, W) token grid per request
+    rows: Tuple[int, ...]            # latent rows of each request on this GPU
+    txt_len: int                     # text tokens per request
+    attn_heads: Optional[int] = None     # heads of the self-attention stage if it differs (SP share)
+    attn_rows: Optional[Tuple[int, ...]] = None  # full request lengths seen by self-attention (SP share)
+    rope_theta: float = 10000.0
+    ln_eps: float = 1e-6
+    rms_eps: float = 1e-6
+    description: str = ""
+
+    @property
+    def n_req(self) -> int:
+        return len(self.rows)
+
+    @property
+    def n_rows(self) -> int:
+        return sum(self.rows)
+
+    @property
+    def n_txt(self) -> int:
+        return self.txt_len * self.n_req
+
+    @property
+    def is_sp_share(self) -> bool:
+        return self.attn_rows is not None
+
+    def cu_seqlens(self) -> List[int]:
+        out = [0]
+        for r in self.rows:
+            out.append(out[-1] + r)
+        return out
+
+    def cu_txt(self) -> List[int]:
+        return [i * self.txt_len for i in range(self.n_req + 1)]
+
+    def cu_attn(self) -> List[int]:
+        rows = self.attn_rows if self.attn_rows is not None else self.rows
+        out = [0]
+        for r in rows:
+            out.append(out[-1] + r)
+        return out
+
+
+def _w(name, wid, dtype, D, H, d, Dff, F, sec, grids, rows, L, desc, **kw):
+    return Workload(name=name, wid=wid, dtype=dtype, hidden=D, n_heads=H, head_dim=d,
+                    mlp_hidden=Dff, freq_dim=F, rope_sections=sec, grids=tuple(grids),
+                    rows=tuple(rows), txt_len=L, description=desc, **kw)
+
+
+WORKLOADS: Dict[str, Workload] = {}
+for _wl in [
+    _w("tiny_image_fp32", 1, "f32", 384, 6, 64, 1536, 384, (0, 32, 32), [(1, 8, 8)], [64], 77,
+       "tiny image block, fp32: 16x16x4 latent, patch 2 -> 64 tokens; D 384, 6x64 heads, "
+       "MLP 1536, 77 text tokens"),
+    _w("image_1024", 2, "bf16", 3072, 24, 128, 12288, 3072, (0, 64, 64), [(1, 64, 64)], [4096], 512,
+       "1024x1024 image block, bf16: 128x128x16 latent, patch 2 -> 4,096 tokens; D 3072, "
+       "24x128 heads, MLP 12288, 512 text tokens"),
+    _w("video_480p", 3, "bf16", 5120, 40, 128, 13824, 5120, (44, 42, 42), [(21, 30, 52)], [32760], 512,
+       "480p video block, bf16: latent 21x60x104x16, patch 1x2x2 -> 32,760 tokens; D 5120, "
+       "40x128 heads, MLP 13824, 512 text tokens"),
+    _w("video_720p", 4, "bf16", 5120, 40, 128, 13824, 5120, (44, 42, 42), [(21, 45, 80)], [75600], 512,
+       "720p video block, bf16: latent 21x90x160x16, patch 1x2x2 -> 75,600 tokens; D 5120, "
+       "40x128 heads, MLP 13824, 512 text tokens"),
+    _w("packed_sp8_share", 5, "bf16", 5120, 40, 128, 13824, 5120, (44, 42, 42),
+       [(1, 64, 64), (1, 96, 96), (21, 30, 52), (21, 45, 80)], [512, 1152, 4095, 9450], 512,
+       "heterogeneous packed batch, one GPU's share at sequence-parallel degree 8: requests of "
+       "4,096 / 9,216 / 32,760 / 75,600 tokens; per-token stages on the first 1/8 of each "
+       "request's rows with all 40 heads; self-attention over the full lengths with 5 of 40 heads",
+       attn_heads=5, attn_rows=(4096, 9216, 32760, 75600)),
+]:
+    WORKLOADS[_wl.name] = _wl
+
+
+def get_workload(name: str) -> Workload:
+    try:
+        return WORKLOADS[name]
+    except KeyError:
+        raise KeyError(f"unknown workload {name!r}; known: {sorted(WORKLOADS)}") from None
