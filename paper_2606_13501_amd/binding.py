@@ -1,0 +1,259 @@
+"""Thin ctypes binding of ``libditblock.so`` (argument marshalling only).
+
+Every function here mirrors one ``extern "C"`` entry point of
+``include/dit_block.h`` under the same name without the ``dit_`` prefix.
+Tensors are torch tensors on the current ROCm device; their data pointers
+and ``torch.cuda.current_stream()`` are passed straight through.  Nothing is
+computed in Python: if the library is missing, every call raises.
+"""
+import ctypes
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libditblock.so")
+
+DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP = 0, -1, -2, -3, -4
+DIT_F32, DIT_BF16 = 0, 1
+EPI_NONE, EPI_GELU_TANH, EPI_RESIDUAL, EPI_GATED_RESIDUAL = 0, 1, 2, 3
+MAX_REQ = 64
+
+WEIGHT_FIELDS = (
+    "w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada",
+    "w_qkv", "b_qkv", "g_q", "g_k", "w_o", "b_o",
+    "g_ca", "b_ca", "w_cq", "b_cq", "w_ckv", "b_ckv", "g_cq", "g_ck", "w_co", "b_co",
+    "w_up", "b_up", "w_dn", "b_dn",
+)
+
+
+class DitError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        self.status = status
+        super().__init__(f"{func}: status {status}: {detail}")
+
+
+class ExtensionMissing(RuntimeError):
+    pass
+
+
+class CConfig(ctypes.Structure):
+    _fields_ = [
+        ("hidden", ctypes.c_int), ("n_heads", ctypes.c_int), ("head_dim", ctypes.c_int),
+        ("mlp_hidden", ctypes.c_int), ("freq_dim", ctypes.c_int),
+        ("rope_sections", ctypes.c_int * 3), ("rope_theta", ctypes.c_float),
+        ("qk_norm", ctypes.c_int), ("ln_eps", ctypes.c_float), ("rms_eps", ctypes.c_float),
+        ("dtype", ctypes.c_int),
+    ]
+
+
+class CWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+
+
+class CVarlen(ctypes.Structure):
+    _fields_ = [
+        ("n_req", ctypes.c_int),
+        ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
+        ("cu_seqlens_txt", ctypes.POINTER(ctypes.c_int32)),
+        ("grid_fhw", ctypes.POINTER(ctypes.c_int32)),
+        ("pos_offset", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ExtensionMissing(f"{LIB_PATH} not found: build it with paper_2606_13501_amd.build.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    PC, PW, PV = ctypes.POINTER(CConfig), ctypes.POINTER(CWeights), ctypes.POINTER(CVarlen)
+    PI = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "dit_block_workspace_size": (sz, [PC, PV]),
+        "dit_block_forward": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_block_pre_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_block_post_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_timestep_modulation": (i32, [PC, PW, i32, vp, vp, vp, sz, vp]),
+        "dit_attention_varlen": (i32, [vp, vp, vp, vp, i64, i64, i64, i64, PI, PI, i32, i32, i32, f32, i32, vp]),
+        "dit_adaln_modulate": (i32, [vp, vp, vp, i64, PI, i32, i32, f32, vp, i32, vp]),
+        "dit_layer_norm_affine": (i32, [vp, vp, vp, i64, i32, f32, vp, i32, vp]),
+        "dit_linear": (i32, [vp, i64, vp, i64, vp, vp, i64, i64, i32, i32, i32, vp, i64, vp, i64, PI, i32, i32, vp]),
+        "dit_qk_norm_rope": (i32, [vp, vp, i64, i64, i32, i32, vp, vp, f32, PI, f32, PV, i32, vp]),
+        "dit_gated_residual": (i32, [vp, vp, vp, vp, i64, PI, i32, i32, vp, i32, vp]),
+        "dit_status_string": (ctypes.c_char_p, [i32]),
+        "dit_last_error": (ctypes.c_char_p, []),
+        "dit_abi_version": (i32, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def exported_symbols() -> Sequence[str]:
+    return [n for n in ("dit_block_workspace_size", "dit_block_forward", "dit_block_pre_attention",
+                        "dit_block_post_attention", "dit_timestep_modulation", "dit_attention_varlen",
+                        "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
+                        "dit_gated_residual", "dit_status_string", "dit_last_error", "dit_abi_version")]
+
+
+def _check(status: int, func: str):
+    if status != DIT_OK:
+        detail = lib().dit_last_error().decode()
+        raise DitError(status, func, detail)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return DIT_BF16
+    if dt == torch.float32:
+        return DIT_F32
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _pi(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+class BlockConfig:
+    """Python view of dit_block_config."""
+
+    def __init__(self, hidden, n_heads, head_dim, mlp_hidden, freq_dim, rope_sections, dtype,
+                 rope_theta=10000.0, qk_norm=True, ln_eps=1e-6, rms_eps=1e-6):
+        self.c = CConfig()
+        self.c.hidden, self.c.n_heads, self.c.head_dim = hidden, n_heads, head_dim
+        self.c.mlp_hidden, self.c.freq_dim = mlp_hidden, freq_dim
+        for i in range(3):
+            self.c.rope_sections[i] = int(rope_sections[i])
+        self.c.rope_theta = rope_theta
+        self.c.qk_norm = 1 if qk_norm else 0
+        self.c.ln_eps, self.c.rms_eps = ln_eps, rms_eps
+        self.c.dtype = dtype_code(dtype) if isinstance(dtype, torch.dtype) else int(dtype)
+
+
+class Varlen:
+    """Python view of dit_varlen; keeps its host arrays alive."""
+
+    def __init__(self, cu_seqlens, cu_txt=None, grid_fhw=None, pos_offset=None):
+        self.cu = _i32(cu_seqlens)
+        self.cu_txt = _i32(cu_txt) if cu_txt is not None else None
+        self.grid = _i32(np.asarray(grid_fhw).reshape(-1)) if grid_fhw is not None else None
+        self.off = _i32(pos_offset) if pos_offset is not None else None
+        self.c = CVarlen()
+        self.c.n_req = len(self.cu) - 1
+        self.c.cu_seqlens = _pi(self.cu)
+        self.c.cu_seqlens_txt = _pi(self.cu_txt)
+        self.c.grid_fhw = _pi(self.grid)
+        self.c.pos_offset = _pi(self.off)
+
+
+def make_weights(w: Dict[str, Optional[torch.Tensor]]) -> CWeights:
+    cw = CWeights()
+    for n in WEIGHT_FIELDS:
+        t = w.get(n)
+        setattr(cw, n, t.data_ptr() if t is not None else None)
+    return cw
+
+
+# ------------------------------------------------------------ entry points
+
+
+def block_workspace_size(cfg: BlockConfig, vl: Varlen) -> int:
+    return int(lib().dit_block_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c)))
+
+
+def block_forward(cfg, weights: CWeights, vl, x, t, txt, y, ws, stream=None):
+    _check(lib().dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
+                                   _ptr(t), _ptr(txt), _ptr(y), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream(stream)), "dit_block_forward")
+
+
+def block_pre_attention(cfg, weights, vl, x, t, mod, qkv, ws, stream=None):
+    _check(lib().dit_block_pre_attention(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
+                                         _ptr(t), _ptr(mod), _ptr(qkv), _ptr(ws), ws.numel() * ws.element_size(),
+                                         _stream(stream)), "dit_block_pre_attention")
+
+
+def block_post_attention(cfg, weights, vl, x, o, txt, mod, y, ws, stream=None):
+    _check(lib().dit_block_post_attention(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
+                                          _ptr(o), _ptr(txt), _ptr(mod), _ptr(y), _ptr(ws),
+                                          ws.numel() * ws.element_size(), _stream(stream)),
+           "dit_block_post_attention")
+
+
+def timestep_modulation(cfg, weights, t, mod, ws, stream=None):
+    _check(lib().dit_timestep_modulation(ctypes.byref(cfg.c), ctypes.byref(weights), int(t.numel()), _ptr(t),
+                                         _ptr(mod), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "dit_timestep_modulation")
+
+
+def attention_varlen(q, k, v, o, cu_q, cu_k, n_heads, head_dim, softmax_scale=None, stream=None):
+    cq, ck = _i32(cu_q), _i32(cu_k)
+    scale = softmax_scale if softmax_scale is not None else head_dim ** -0.5
+    _check(lib().dit_attention_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(o), q.stride(0), k.stride(0), v.stride(0),
+                                      o.stride(0), _pi(cq), _pi(ck), len(cq) - 1, n_heads, head_dim, scale,
+                                      dtype_code(q.dtype), _stream(stream)), "dit_attention_varlen")
+
+
+def adaln_modulate(x, shift, scale, mod_stride, cu_seqlens, eps, out, stream=None):
+    cu = _i32(cu_seqlens)
+    _check(lib().dit_adaln_modulate(_ptr(x), _ptr(shift), _ptr(scale), mod_stride, _pi(cu), len(cu) - 1,
+                                    x.shape[-1], eps, _ptr(out), dtype_code(x.dtype), _stream(stream)),
+           "dit_adaln_modulate")
+
+
+def layer_norm_affine(x, gamma, beta, eps, out, stream=None):
+    _check(lib().dit_layer_norm_affine(_ptr(x), _ptr(gamma), _ptr(beta), x.shape[0], x.shape[-1], eps, _ptr(out),
+                                       dtype_code(x.dtype), _stream(stream)), "dit_layer_norm_affine")
+
+
+def linear(a, w, bias, out, epi=EPI_NONE, res=None, gate=None, gate_stride=0, cu_seqlens=None, stream=None):
+    cu = _i32(cu_seqlens) if cu_seqlens is not None else None
+    _check(lib().dit_linear(_ptr(a), a.stride(0), _ptr(w), w.stride(0), _ptr(bias), _ptr(out), out.stride(0),
+                            a.shape[0], w.shape[0], a.shape[1], epi, _ptr(res), res.stride(0) if res is not None else 0,
+                            _ptr(gate), gate_stride, _pi(cu), (len(cu) - 1) if cu is not None else 0,
+                            dtype_code(a.dtype), _stream(stream)), "dit_linear")
+
+
+def qk_norm_rope(q, k, n_heads, head_dim, g_q, g_k, eps, rope_sections=(0, 0, 0), rope_theta=10000.0,
+                 vl: Optional[Varlen] = None, stream=None):
+    sec = (ctypes.c_int * 3)(*[int(s) for s in rope_sections])
+    _check(lib().dit_qk_norm_rope(_ptr(q), _ptr(k), q.stride(0), q.shape[0], n_heads, head_dim, _ptr(g_q), _ptr(g_k),
+                                  eps, ctypes.cast(sec, ctypes.POINTER(ctypes.c_int32)), rope_theta,
+                                  ctypes.byref(vl.c) if vl is not None else None, dtype_code(q.dtype),
+                                  _stream(stream)), "dit_qk_norm_rope")
+
+
+def gated_residual(x, z, bias, gate, gate_stride, cu_seqlens, out, stream=None):
+    cu = _i32(cu_seqlens)
+    _check(lib().dit_gated_residual(_ptr(x), _ptr(z), _ptr(bias), _ptr(gate), gate_stride, _pi(cu), len(cu) - 1,
+                                    x.shape[-1], _ptr(out), dtype_code(x.dtype), _stream(stream)),
+           "dit_gated_residual")

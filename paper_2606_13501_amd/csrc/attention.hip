@@ -1,0 +1,347 @@
+// Scaled dot-product attention over a packed batch, non-causal (the denoising
+// step attends bidirectionally over the whole latent sequence).
+//
+// bf16, head_dim 128: flash-style kernel for gfx950.  One 512-thread workgroup
+// (8 waves, 2 per SIMD) owns 256 query rows of one (request, head); each wave
+// owns 32 of them.  K and V tiles of 64 keys are staged through LDS (two
+// stages; V is stored transposed, d-major).  Per tile a wave computes
+// S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K as the A operand), so that every
+// lane holds 16 scores of ONE query row: the running max and sum of that row
+// live in the lane, P^T feeds the next MFMA straight from the lane's registers,
+// and O^T = V^T P^T leaves the output of the same query row in the same lane.
+// The key order inside each 32-key block is permuted (bits 2 and 3 of the key
+// index swapped) so that the 8 keys a lane contributes to a PV MFMA are
+// contiguous in the transposed V tile (one 16-byte LDS read).  Softmax runs in
+// fp32 with exp2 and the log2(e) folded into the scale; P is rounded to bf16
+// for the PV product.
+//
+// fp32: one thread per (query row, head) with an exact online softmax.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace dit {
+
+namespace {
+
+constexpr int D = 128;           // head_dim of the bf16 kernel
+constexpr int BQ = 256;          // query rows per workgroup
+constexpr int BKV = 64;          // keys per LDS tile
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kKBytes = BKV * D * 2;     // 16 KiB
+constexpr int kVBytes = BKV * D * 2;     // 16 KiB
+constexpr int kStage = kKBytes + kVBytes;
+constexpr int kXcds = 8;
+
+struct AttnWork {
+  int n_req;                        // requests, in scheduling order (longest first)
+  int q_start[DIT_MAX_REQ];
+  int q_len[DIT_MAX_REQ];
+  int k_start[DIT_MAX_REQ];
+  int k_len[DIT_MAX_REQ];
+  int tiles_q[DIT_MAX_REQ];         // query tiles of one head
+  int prefix[DIT_MAX_REQ + 1];      // work items before request i (all heads)
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+
+// swap bits 2 and 3 of a key index inside its 16-key group
+__device__ __forceinline__ int perm23(int x) {
+  return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
+    float scale_log2, AttnWork work) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+
+  // ---- work item: XCD-contiguous numbering, requests longest first
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const int w = (b % kXcds) * (nb / kXcds) + b / kXcds;
+  if (w >= work.prefix[work.n_req]) return;
+  int r = 0;
+  while (w >= work.prefix[r + 1]) ++r;
+  const int local = w - work.prefix[r];
+  const int head = local / work.tiles_q[r];
+  const int qt = local - head * work.tiles_q[r];
+  const int q0 = work.q_start[r] + qt * BQ;
+  const int q_end = work.q_start[r] + work.q_len[r];
+  const int k0 = work.k_start[r];
+  const int n_k = work.k_len[r];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int fr = lane & 31;
+  const int fh = lane >> 5;
+
+  // ---- Q fragments (MFMA B operand of S^T): row fr of this wave, d 16kk + 8fh .. +7
+  const int my_q = q0 + wave * 32 + fr;
+  bf16x8 qf[8];
+  {
+    const int qrow = min(my_q, q_end - 1);
+    const bf16* qp = Q + (int64_t)qrow * qs + head * D + 8 * fh;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + 16 * kk);
+  }
+
+  // ---- global -> LDS staging
+  // K: 2 chunks of 16 B per thread: key = (tid >> 4) + 32 i, chunk c = tid & 15
+  // buffer resources are rebased at every tile so offsets stay small; loads
+  // past the request's last key return zeros
+  const bf16* k_head = K + (int64_t)k0 * ks + head * D;
+  const bf16* v_head = V + (int64_t)k0 * vs + head * D;
+  const int kl_key = tid >> 4;
+  const int kl_c = tid & 15;
+  const int kl_voff = kl_key * (int)ks * 2 + kl_c * 16;
+  int kl_st[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    int key = kl_key + 32 * i;
+    kl_st[i] = key * 256 + ((kl_c ^ perm23(key & 15)) << 4);
+  }
+  // V: keys 4 kg .. 4 kg + 3, d 4 dc .. 4 dc + 3 (8-byte loads), written as V^T
+  const int vl_lo = tid & 1;
+  const int vl_dc = (tid >> 1) & 31;
+  const int vl_kg = 2 * (tid >> 6) + vl_lo;
+  const int vl_voff = (4 * vl_kg) * (int)vs * 2 + vl_dc * 8;
+  int vl_st[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    int d = 4 * vl_dc + e;
+    int c = vl_kg >> 1;
+    vl_st[e] = d * 128 + ((c ^ ((d ^ (d >> 3)) & 7)) << 4) + (vl_kg & 1) * 8;
+  }
+
+  u32x4 kreg[2];
+  u32x2 vreg[4];
+  auto gload = [&](int kt) {
+    const int kb0 = kt * BKV;
+    const __amdgpu_buffer_rsrc_t k_rs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
+    const __amdgpu_buffer_rsrc_t v_rs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(k_rs, kl_voff, 32 * i * (int)ks * 2, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      vreg[i] = __builtin_amdgcn_raw_buffer_load_b64(v_rs, vl_voff, i * (int)vs * 2, 0);
+    // keys past the request end: zero V so that P = 0 times V stays exact
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (kb0 + 4 * vl_kg + i >= n_k) vreg[i] = u32x2{0u, 0u};
+  };
+  auto sstore = [&](int stage) {
+    char* kb = smem + stage * kStage;
+    char* vb = kb + kKBytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st[i]) = kreg[i];
+    // transpose 4 keys x 4 d: element (key i, d e) -> V^T[d e][key i]
+    const uint16_t* vv = reinterpret_cast<const uint16_t*>(vreg);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      u32x2 t;
+      t[0] = (uint32_t)vv[0 * 4 + e] | ((uint32_t)vv[1 * 4 + e] << 16);
+      t[1] = (uint32_t)vv[2 * 4 + e] | ((uint32_t)vv[3 * 4 + e] << 16);
+      *reinterpret_cast<u32x2*>(vb + vl_st[e]) = t;
+    }
+  };
+
+  // ---- fragment read offsets
+  // K (A operand of S^T): key 32 kb + perm23(fr), chunk 2 kk + fh
+  const int kf_key = perm23(fr);
+  const int kf_base = kf_key * 256;
+  const int kf_sw = perm23(kf_key & 15);   // == fr & 15
+  // V^T (A operand of O^T): row d = 32 dblk + fr, chunk 4 kb + 2 s + fh
+  int vf_sw[4];   // (d ^ (d >> 3)) & 7 with d = 32 dblk + fr
+#pragma unroll
+  for (int dblk = 0; dblk < 4; ++dblk) vf_sw[dblk] = (fr ^ (4 * dblk + (fr >> 3))) & 7;
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) oacc[i] = f32x16{};
+  float m_run = -INFINITY;   // running max of (score * scale_log2)
+  float l_run = 0.f;         // this lane's share of the running sum
+
+  const int n_tiles = (n_k + BKV - 1) / BKV;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < n_tiles) gload(kt + 1);
+    const char* kb = smem + cur * kStage;
+    const char* vb = kb + kKBytes;
+
+    // S^T for 2 blocks of 32 keys: s[kb][4i + j] = S[q = fr][key 32 kb + 8 i + 4 fh + j]
+    // (key order inside a 32-key block: row rho of the MFMA is key perm23(rho))
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const int c = 2 * kk + fh;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + blk * 32 * 256 + kf_base + ((c ^ kf_sw) << 4));
+        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[blk], 0, 0, 0);
+      }
+    }
+
+    // mask keys past the request end (only the last tile can have them)
+    const int kbase = kt * BKV;
+    if (kbase + BKV > n_k) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          int key = kbase + 32 * blk + perm23(8 * (v >> 2) + 4 * fh + (v & 3));
+          if (key >= n_k) s[blk][v] = -INFINITY;
+        }
+    }
+
+    // online softmax for query row fr (the other half-wave holds the other keys)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[blk][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx * scale_log2);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale_log2, -m_new));
+        psum += p;
+        pf[blk][v >> 3][v & 7] = (bf16)p;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
+
+    // O^T += V^T P^T: 4 d-blocks x (2 key blocks x 2 halves of 16 keys)
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int hs = 0; hs < 2; ++hs) {
+        const int c = 4 * blk + 2 * hs + fh;
+#pragma unroll
+        for (int dblk = 0; dblk < 4; ++dblk) {
+          const int d = 32 * dblk + fr;
+          bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + d * 128 + ((c ^ vf_sw[dblk]) << 4));
+          oacc[dblk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[blk][hs], oacc[dblk], 0, 0, 0);
+        }
+      }
+
+    if (kt + 1 < n_tiles) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- normalise and store: oacc[dblk][4i + j] = O[q = fr][d = 32 dblk + 8 i + 4 fh + j]
+  // (the S^T rows of a lane are keys perm23(8 i + 4 fh + j); for the PV MFMA of
+  // half hs the lane's 8 values are keys 16 hs + 8 fh + 0..7 of the block)
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
+  if (my_q < q_end) {
+    bf16* op = O + (int64_t)my_q * os + head * D + 4 * fh;
+#pragma unroll
+    for (int dblk = 0; dblk < 4; ++dblk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bf16x4 ov;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ov[j] = (bf16)(oacc[dblk][4 * i + j] * inv);
+        *reinterpret_cast<bf16x4*>(op + 32 * dblk + 8 * i) = ov;
+      }
+  }
+}
+
+// ------------------------------------------------------------------- fp32
+
+__global__ __launch_bounds__(64) void attn_fwd_f32(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    float* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads, int head_dim,
+    float scale, ReqTable cq, ReqTable ck, int n_q) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_q * n_heads) return;
+  const int row = idx / n_heads;
+  const int head = idx - row * n_heads;
+  const int r = find_req(cq.cu, cq.n_req, row);
+  const int kb = ck.cu[r], ke = ck.cu[r + 1];
+  const float* q = Q + (int64_t)row * qs + head * head_dim;
+  float m = -INFINITY, l = 0.f;
+  float acc[128];
+  for (int e = 0; e < head_dim; ++e) acc[e] = 0.f;
+  for (int j = kb; j < ke; ++j) {
+    const float* k = K + (int64_t)j * ks + head * head_dim;
+    float s = 0.f;
+    for (int e = 0; e < head_dim; ++e) s = fmaf(q[e], k[e], s);
+    s *= scale;
+    float m_new = fmaxf(m, s);
+    float a = expf(m - m_new);
+    float p = expf(s - m_new);
+    l = l * a + p;
+    const float* v = V + (int64_t)j * vs + head * head_dim;
+    for (int e = 0; e < head_dim; ++e) acc[e] = acc[e] * a + p * v[e];
+    m = m_new;
+  }
+  float* o = O + (int64_t)row * os + head * head_dim;
+  const float inv = ke > kb ? 1.0f / l : 0.f;
+  for (int e = 0; e < head_dim; ++e) o[e] = acc[e] * inv;
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
+  const int n_req = p.cq.n_req;
+  if (p.dtype == DIT_F32) {
+    const int n_q = p.cq.cu[n_req];
+    if (n_q == 0) return hipSuccess;
+    const int total = n_q * p.n_heads;
+    attn_fwd_f32<<<(total + 63) / 64, 64, 0, s>>>(
+        (const float*)p.q, (const float*)p.k, (const float*)p.v, (float*)p.o, p.q_stride, p.k_stride,
+        p.v_stride, p.o_stride, p.n_heads, p.head_dim, p.scale, p.cq, p.ck, n_q);
+    return hipGetLastError();
+  }
+  // requests with queries, longest key range first (their tiles do the most work)
+  AttnWork w{};
+  int order[DIT_MAX_REQ];
+  int n = 0;
+  for (int r = 0; r < n_req; ++r)
+    if (p.cq.cu[r + 1] > p.cq.cu[r]) order[n++] = r;
+  for (int i = 1; i < n; ++i) {
+    int x = order[i], j = i - 1;
+    int lx = p.ck.cu[x + 1] - p.ck.cu[x];
+    while (j >= 0 && (p.ck.cu[order[j] + 1] - p.ck.cu[order[j]]) < lx) { order[j + 1] = order[j]; --j; }
+    order[j + 1] = x;
+  }
+  w.n_req = n;
+  w.prefix[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    int r = order[i];
+    w.q_start[i] = p.cq.cu[r];
+    w.q_len[i] = p.cq.cu[r + 1] - p.cq.cu[r];
+    w.k_start[i] = p.ck.cu[r];
+    w.k_len[i] = p.ck.cu[r + 1] - p.ck.cu[r];
+    w.tiles_q[i] = (w.q_len[i] + BQ - 1) / BQ;
+    w.prefix[i + 1] = w.prefix[i] + w.tiles_q[i] * p.n_heads;
+  }
+  const int items = w.prefix[n];
+  if (items == 0) return hipSuccess;
+  const int grid = (items + kXcds - 1) / kXcds * kXcds;
+  const float scale_log2 = p.scale * 1.4426950408889634f;
+  attn_fwd_bf16<<<grid, kThreads, 0, s>>>((const bf16*)p.q, (const bf16*)p.k, (const bf16*)p.v,
+                                          (bf16*)p.o, p.q_stride, p.k_stride, p.v_stride, p.o_stride,
+                                          p.n_heads, scale_log2, w);
+  return hipGetLastError();
+}
+
+}  // namespace dit

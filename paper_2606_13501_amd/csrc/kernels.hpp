@@ -1,0 +1,88 @@
+// Host-side launchers of the gfx950 kernels (arguments are validated by the
+// C-ABI layer before any of these is called).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "dit_block.h"
+
+namespace dit {
+
+struct LinearArgs {
+  const void* a; int64_t lda;
+  const void* w; int64_t ldw;
+  const void* bias;
+  void* out; int64_t ldo;
+  int64_t M; int N; int K;
+  dit_epilogue epi;
+  const void* res; int64_t ldr;
+  const float* gate; int64_t gate_stride;
+  ReqTable req;
+  dit_dtype dtype;
+};
+hipError_t launch_linear(const LinearArgs& p, hipStream_t s);
+
+struct AttnArgs {
+  const void *q, *k, *v;
+  void* o;
+  int64_t q_stride, k_stride, v_stride, o_stride;  // elements
+  ReqTable cq, ck;
+  int n_heads, head_dim;
+  float scale;
+  dit_dtype dtype;
+};
+hipError_t launch_attention(const AttnArgs& p, hipStream_t s);
+
+// out = LN(x) * mul + add, mul/add per request (modulate: mul = 1 + scale) or
+// shared (affine: gamma, beta).
+struct LnArgs {
+  const void* x;
+  void* out;
+  int64_t n_rows;
+  int hidden;
+  float eps;
+  bool affine;
+  const float* shift; const float* scale; int64_t mod_stride;  // modulate
+  const void* gamma; const void* beta;                          // affine
+  ReqTable req;
+  dit_dtype dtype;
+};
+hipError_t launch_layer_norm(const LnArgs& p, hipStream_t s);
+
+struct NormRopeArgs {
+  void* q; void* k;
+  int64_t row_stride, n_rows;
+  int n_heads, head_dim;
+  const void* g_q; const void* g_k;
+  float eps;
+  bool rope;
+  int sections[3];
+  float theta;
+  RopeTable tab;
+  dit_dtype dtype;
+};
+hipError_t launch_qk_norm_rope(const NormRopeArgs& p, hipStream_t s);
+
+struct GatedResArgs {
+  const void* x; const void* z; const void* bias;
+  const float* gate; int64_t gate_stride;
+  void* out;
+  int64_t n_rows; int hidden;
+  ReqTable req;
+  dit_dtype dtype;
+};
+hipError_t launch_gated_residual(const GatedResArgs& p, hipStream_t s);
+
+// Timestep conditioning: e (fp32 [R,F]) -> ... -> mod (fp32 [R,6D]).
+struct CondArgs {
+  const float* t; int n_req; int freq_dim; int hidden;
+  const void *w_t1, *b_t1, *w_t2, *b_t2, *w_ada, *b_ada;
+  float* e; float* a1; float* c;   // scratch [R,F], [R,D], [R,D]
+  float* mod;
+  dit_dtype dtype;
+};
+hipError_t launch_conditioning(const CondArgs& p, hipStream_t s);
+
+}  // namespace dit

@@ -6,12 +6,12 @@ read the exact same stored bits from here.
 """
 from .workloads import Workload, WORKLOADS, get_workload
 from .gen import (
-    bf16_bits, generate_block_inputs, generate_tensor, TensorSpec,
+    bf16_bits, generate_block_inputs, generate_tensor, TensorSpec, draw,
     block_tensor_specs, generate_attention_inputs, generate_sampled_rows,
 )
 
 __all__ = [
     "Workload", "WORKLOADS", "get_workload", "bf16_bits", "generate_block_inputs",
     "generate_tensor", "TensorSpec", "block_tensor_specs",
-    "generate_attention_inputs", "generate_sampled_rows",
+    "generate_attention_inputs", "generate_sampled_rows", "draw",
 ]

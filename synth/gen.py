@@ -9,9 +9,10 @@ Recipe (one fixed draw per named tensor, independent of generation order):
 * standard normal draws in float32, scaled by the tensor's std and shifted by
   its mean, then stored either as float32 or as bfloat16 bits obtained by
   round-to-nearest-even on the float32 bit pattern;
-* latents and text embeddings ~ N(0, 1); Linear weights and biases
-  ~ N(0, 0.02^2); norm gains ~ 1 + N(0, 0.02^2); LayerNorm shift ~ N(0, 0.02^2);
-  timesteps ~ U[0, 1000) (float32).
+* latents and text embeddings ~ N(0, 1); Linear weight matrices
+  ~ N(0, linear_std^2) (0.02 for every workload shaped like the paper's);
+  biases ~ N(0, 0.02^2); norm gains ~ 1 + N(0, 0.02^2); LayerNorm shift
+  ~ N(0, 0.02^2); timesteps ~ U[0, 1000) (float32).
 
 bfloat16 values travel as ``uint16`` arrays of their bit patterns.
 """
@@ -93,37 +94,37 @@ def generate_tensor(spec: TensorSpec, wl: Workload, threads: Optional[int] = Non
 def block_tensor_specs(wl: Workload) -> Dict[str, TensorSpec]:
     """All inputs and weights of one block, keyed by name ([out, in] weights)."""
     D, F, Dff, d = wl.hidden, wl.freq_dim, wl.mlp_hidden, wl.head_dim
-    W = 0.02
+    W = wl.linear_std
     specs = [
         TensorSpec("x", 1, (wl.n_rows, D), "normal"),
         TensorSpec("txt", 2, (wl.n_txt, D), "normal"),
         TensorSpec("t", 3, (wl.n_req,), "uniform", lo=0.0, hi=1000.0, dtype="f32"),
         TensorSpec("w_t1", 10, (D, F), "normal", std=W),
-        TensorSpec("b_t1", 11, (D,), "normal", std=W),
+        TensorSpec("b_t1", 11, (D,), "normal", std=0.02),
         TensorSpec("w_t2", 12, (D, D), "normal", std=W),
-        TensorSpec("b_t2", 13, (D,), "normal", std=W),
+        TensorSpec("b_t2", 13, (D,), "normal", std=0.02),
         TensorSpec("w_ada", 14, (6 * D, D), "normal", std=W),
-        TensorSpec("b_ada", 15, (6 * D,), "normal", std=W),
+        TensorSpec("b_ada", 15, (6 * D,), "normal", std=0.02),
         TensorSpec("w_qkv", 16, (3 * D, D), "normal", std=W),
-        TensorSpec("b_qkv", 17, (3 * D,), "normal", std=W),
-        TensorSpec("g_q", 18, (d,), "normal", mean=1.0, std=W),
-        TensorSpec("g_k", 19, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("b_qkv", 17, (3 * D,), "normal", std=0.02),
+        TensorSpec("g_q", 18, (d,), "normal", mean=1.0, std=0.02),
+        TensorSpec("g_k", 19, (d,), "normal", mean=1.0, std=0.02),
         TensorSpec("w_o", 20, (D, D), "normal", std=W),
-        TensorSpec("b_o", 21, (D,), "normal", std=W),
-        TensorSpec("g_ca", 22, (D,), "normal", mean=1.0, std=W),
-        TensorSpec("b_ca", 23, (D,), "normal", std=W),
+        TensorSpec("b_o", 21, (D,), "normal", std=0.02),
+        TensorSpec("g_ca", 22, (D,), "normal", mean=1.0, std=0.02),
+        TensorSpec("b_ca", 23, (D,), "normal", std=0.02),
         TensorSpec("w_cq", 24, (D, D), "normal", std=W),
-        TensorSpec("b_cq", 25, (D,), "normal", std=W),
+        TensorSpec("b_cq", 25, (D,), "normal", std=0.02),
         TensorSpec("w_ckv", 26, (2 * D, D), "normal", std=W),
-        TensorSpec("b_ckv", 27, (2 * D,), "normal", std=W),
-        TensorSpec("g_cq", 28, (d,), "normal", mean=1.0, std=W),
-        TensorSpec("g_ck", 29, (d,), "normal", mean=1.0, std=W),
+        TensorSpec("b_ckv", 27, (2 * D,), "normal", std=0.02),
+        TensorSpec("g_cq", 28, (d,), "normal", mean=1.0, std=0.02),
+        TensorSpec("g_ck", 29, (d,), "normal", mean=1.0, std=0.02),
         TensorSpec("w_co", 30, (D, D), "normal", std=W),
-        TensorSpec("b_co", 31, (D,), "normal", std=W),
+        TensorSpec("b_co", 31, (D,), "normal", std=0.02),
         TensorSpec("w_up", 32, (Dff, D), "normal", std=W),
-        TensorSpec("b_up", 33, (Dff,), "normal", std=W),
+        TensorSpec("b_up", 33, (Dff,), "normal", std=0.02),
         TensorSpec("w_dn", 34, (D, Dff), "normal", std=W),
-        TensorSpec("b_dn", 35, (D,), "normal", std=W),
+        TensorSpec("b_dn", 35, (D,), "normal", std=0.02),
     ]
     return {s.name: s for s in specs}
 
@@ -185,3 +186,32 @@ def generate_sampled_rows(wl: Workload, n_per_req: int, sample_id: int = 0,
         rows = np.unique(np.concatenate([np.array(must, dtype=np.int64), pick.astype(np.int64)]))
         out.append(rows + cu[r])
     return np.concatenate(out)
+
+
+def draw(shape, key: Sequence[int], dtype: str = "bf16", dist: str = "normal", mean: float = 0.0,
+         std: float = 1.0, lo: float = 0.0, hi: float = 1.0, threads: Optional[int] = None) -> np.ndarray:
+    """A free-standing seeded tensor (same recipe, seed [13501, 900, *key, chunk])."""
+    class _W:
+        wid = 900
+    spec = TensorSpec("draw", 0, tuple(int(s) for s in shape), dist, mean=mean, std=std, lo=lo, hi=hi)
+    threads = threads or min(16, os.cpu_count() or 1)
+    n = int(np.prod(spec.shape)) if spec.shape else 1
+    out = np.empty(n, dtype=np.uint16 if dtype == "bf16" else np.float32)
+    chunks = [(c, c * CHUNK, min(n, (c + 1) * CHUNK)) for c in range((n + CHUNK - 1) // CHUNK)]
+
+    def work(ch):
+        c, a, b = ch
+        rng = np.random.default_rng([SEED, 900] + [int(k) for k in key] + [c])
+        if dist == "normal":
+            v = rng.standard_normal(b - a, dtype=np.float32) * np.float32(std) + np.float32(mean)
+        else:
+            v = (rng.random(b - a, dtype=np.float32) * np.float32(hi - lo) + np.float32(lo)).astype(np.float32)
+        out[a:b] = bf16_bits(v) if dtype == "bf16" else v
+
+    if len(chunks) > 1 and threads > 1:
+        with ThreadPoolExecutor(min(threads, len(chunks))) as ex:
+            list(ex.map(work, chunks))
+    else:
+        for ch in chunks:
+            work(ch)
+    return out.reshape(spec.shape)

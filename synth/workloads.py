@@ -38,6 +38,7 @@ class Workload:
     rope_theta: float = 10000.0
     ln_eps: float = 1e-6
     rms_eps: float = 1e-6
+    linear_std: float = 0.02         # std of the Linear weight matrices
     description: str = ""
 
     @property

@@ -1,0 +1,159 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dit_block.h")
+
+B = pytest.importorskip("paper_2606_13501_amd.binding")
+
+
+def _lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libditblock.so not built")
+    return B.lib()
+
+
+def header_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(dit_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_header_declares_expected_entry_points():
+    fns = header_functions()
+    for need in ("dit_block_forward", "dit_attention_varlen", "dit_adaln_modulate"):
+        assert need in fns
+
+
+def test_library_exports_every_header_function():
+    _lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (dit_[a-z_0-9]+)", out))
+    missing = [f for f in header_functions() if f not in exported]
+    assert not missing, f"declared but not exported: {missing}"
+    assert sorted(header_functions()) == sorted(B.exported_symbols())
+
+
+def test_abi_version_and_strings():
+    L = _lib()
+    assert L.dit_abi_version() == 1
+    assert L.dit_status_string(B.DIT_ERR_WORKSPACE) == b"workspace too small"
+    assert L.dit_status_string(B.DIT_OK) == b"ok"
+
+
+# Fake, aligned, never-dereferenced device addresses: every call below must
+# fail validation on the host before it could reach a kernel.
+P = ctypes.c_void_p(0x10000)
+P_MIS = ctypes.c_void_p(0x10008)
+
+
+def _cu(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def test_attention_rejects_bad_arguments():
+    L = _lib()
+    cu, pcu = _cu([0, 10])
+    bad, pbad = _cu([0, 10, 5])
+    nz, pnz = _cu([1, 10])
+    S = ctypes.c_void_p(0)
+    call = lambda q, pq, pk, n_req, H, d, scale, dt, qs=128: L.dit_attention_varlen(
+        q, P, P, P, qs, 128, 128, 128, pq, pk, n_req, H, d, scale, dt, S)
+    assert call(None, pcu, pcu, 1, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert b"q is NULL" in L.dit_last_error()
+    assert call(P_MIS, pcu, pcu, 1, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert b"aligned" in L.dit_last_error()
+    assert call(P, pbad, pbad, 2, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert b"decreases" in L.dit_last_error()
+    assert call(P, pnz, pnz, 1, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 0, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 65, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 1, 1, 64, 0.1, B.DIT_BF16) == B.DIT_ERR_UNSUPPORTED
+    assert call(P, pcu, pcu, 1, 1, 96, 0.1, B.DIT_F32) == B.DIT_ERR_UNSUPPORTED
+    assert call(P, pcu, pcu, 1, 2, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG   # stride < H*d
+    assert call(P, pcu, pcu, 1, 1, 128, 0.0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 1, 1, 128, 0.1, 7) == B.DIT_ERR_INVALID_ARG
+
+
+def test_linear_rejects_bad_arguments():
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cu, pcu = _cu([0, 5, 12])
+    f = lambda a, lda, M, N, K, epi, res, gate, pc, nreq, dt: L.dit_linear(
+        a, lda, P, K, None, P, N, M, N, K, epi, res, N, gate, 0, pc, nreq, dt, S)
+    assert f(P, 100, 12, 64, 100, B.EPI_NONE, None, None, None, 0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG  # lda % 8
+    assert f(P, 96, 12, 64, 96, B.EPI_NONE, None, None, None, 0, B.DIT_BF16) == B.DIT_ERR_UNSUPPORTED   # K % 64
+    assert f(P, 128, 12, 64, 128, B.EPI_RESIDUAL, None, None, None, 0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert f(P, 128, 12, 64, 128, B.EPI_GATED_RESIDUAL, P, None, pcu, 2, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert f(P, 128, 13, 64, 128, B.EPI_GATED_RESIDUAL, P, P, pcu, 2, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert b"cu_seqlens ends" in L.dit_last_error()
+    assert f(P, 128, 12, 64, 128, 9, None, None, None, 0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+
+
+def test_norm_kernels_reject_bad_arguments():
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cu, pcu = _cu([0, 4])
+    assert L.dit_adaln_modulate(P, P, P, 3, pcu, 1, 64, 1e-6, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_adaln_modulate(P, P, P, 64, pcu, 1, 60, 1e-6, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_adaln_modulate(P, P, P, 64, pcu, 1, 16384, 1e-6, P, B.DIT_BF16, S) == B.DIT_ERR_UNSUPPORTED
+    assert L.dit_adaln_modulate(P, P, P, 64, pcu, 1, 64, 0.0, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_layer_norm_affine(P, None, P, 4, 64, 1e-6, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    sec = (ctypes.c_int * 3)(44, 42, 40)
+    psec = ctypes.cast(sec, ctypes.POINTER(ctypes.c_int32))
+    assert L.dit_qk_norm_rope(P, P, 256, 4, 2, 128, P, P, 1e-6, psec, 1e4, None, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert b"sum to" in L.dit_last_error()
+    sec = (ctypes.c_int * 3)(43, 43, 42)
+    psec = ctypes.cast(sec, ctypes.POINTER(ctypes.c_int32))
+    assert L.dit_qk_norm_rope(P, P, 256, 4, 2, 128, P, P, 1e-6, psec, 1e4, None, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_qk_norm_rope(P, P, 256, 4, 2, 96, P, P, 1e-6, None, 1e4, None, B.DIT_BF16, S) == B.DIT_ERR_UNSUPPORTED
+    assert L.dit_gated_residual(P, P, None, P, 2, pcu, 1, 64, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+
+
+def _block_structs(dtype=B.DIT_BF16, hidden=256, heads=2, head_dim=128, sections=(0, 64, 64)):
+    cfg = B.BlockConfig(hidden, heads, head_dim, 512, hidden, sections, dtype)
+    w = B.CWeights()
+    for n in B.WEIGHT_FIELDS:
+        setattr(w, n, 0x10000)
+    vl = B.Varlen([0, 16, 40], [0, 8, 20], [(1, 4, 4), (1, 4, 6)])
+    return cfg, w, vl
+
+
+def test_block_validation_and_workspace():
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cfg, w, vl = _block_structs()
+    need = L.dit_block_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c))
+    assert need > 0 and need % 256 == 0
+    # workspace too small, misaligned, missing
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P,
+                            ctypes.c_void_p(0x100000), need - 256, S)
+    assert r == B.DIT_ERR_WORKSPACE
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P,
+                            ctypes.c_void_p(0x100010), need, S)
+    assert r == B.DIT_ERR_WORKSPACE
+    # a weight missing
+    w.w_up = None
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P, P, need, S)
+    assert r == B.DIT_ERR_INVALID_ARG and b"w_up" in L.dit_last_error()
+    # bad configs
+    for kw, code in [(dict(head_dim=64, heads=4, sections=(0, 32, 32)), B.DIT_ERR_UNSUPPORTED),
+                     (dict(sections=(0, 64, 62)), B.DIT_ERR_INVALID_ARG),
+                     (dict(hidden=250), B.DIT_ERR_INVALID_ARG)]:
+        cfg2, w2, vl2 = _block_structs(**kw)
+        r = L.dit_block_forward(ctypes.byref(cfg2.c), ctypes.byref(w2), ctypes.byref(vl2.c), P, P, P, P, P, 1 << 40, S)
+        assert r == code, (kw, r, L.dit_last_error())
+        assert L.dit_block_workspace_size(ctypes.byref(cfg2.c), ctypes.byref(vl2.c)) == 0
+    # rows of a request that do not fit its grid
+    cfg, w, vl = _block_structs()
+    vl = B.Varlen([0, 17, 40], [0, 8, 20], [(1, 4, 4), (1, 4, 6)])
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P, P, 1 << 40, S)
+    assert r == B.DIT_ERR_INVALID_ARG and b"exceed its grid" in L.dit_last_error()

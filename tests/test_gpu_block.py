@@ -1,0 +1,132 @@
+"""Whole-block parity of the HIP path against the CPU oracle (C ABI), plus
+the block's invariants run on the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from synth.workloads import Workload
+from oracle import dit_block as O
+from gpu_util import DeviceBlock, require_gpu, dev, host, empty, check, log
+
+pytestmark = pytest.mark.gpu
+
+# A small packed bf16 batch: three requests with ragged lengths, different
+# grids and text lengths, 3D rotary.  Its Linear weights have std
+# 0.02 * sqrt(5120 / 512) so that activations and adaLN gates have the
+# magnitudes of the D = 5120 video block (gates ~0.7).  With plain 0.02 at
+# D = 512 the gates are ~0.03, y - x is ~50x smaller than y, and rounding the
+# exact result once to bf16 already costs cos(y - x) = 0.9994.
+SMALL_PACKED = Workload(
+    name="small_packed_bf16", wid=50, dtype="bf16", hidden=512, n_heads=4, head_dim=128, mlp_hidden=1024,
+    freq_dim=512, rope_sections=(44, 42, 42), grids=((2, 10, 16), (1, 7, 11), (3, 9, 19)), rows=(300, 77, 513),
+    txt_len=64, linear_std=0.02 * (5120 / 512) ** 0.5, description="small packed bf16 batch for parity")
+
+
+def _oracle_block(db: DeviceBlock, x=None):
+    wl = db.wl
+    w = db.oracle_weights()
+    cfg = O.config_from_workload(wl)
+    vl = O.varlen_from_workload(wl)
+    xx = w["x"] if x is None else x
+    return O.block_forward(cfg, vl, xx, w["t"], w["txt"], w)
+
+
+@pytest.mark.parametrize("name", ["tiny_image_fp32", "image_1024", "small_packed_bf16"])
+def test_block_parity(name):
+    wl = SMALL_PACKED if name == "small_packed_bf16" else synth.get_workload(name)
+    log(f"case block parity {name}")
+    db = DeviceBlock(wl)
+    y = db.forward()
+    torch.cuda.synchronize()
+    g = host(y)
+    ref = _oracle_block(db)
+    x = O.decode(db.inp["x"])
+    check(g, ref, wl.dtype, f"{name} y")
+    check(g - x, ref - x, wl.dtype, f"{name} y - x")
+
+
+def test_block_seams_compose_to_forward():
+    """pre_attention -> attention -> post_attention == block_forward, bitwise."""
+    wl = SMALL_PACKED
+    log("case seams compose")
+    db = DeviceBlock(wl)
+    B = db.B
+    y_ref = db.forward()
+    T, D = wl.n_rows, wl.hidden
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    qkv = empty((T, 3 * D), "bf16")
+    B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, qkv, db.ws)
+    o = empty((T, D), "bf16")
+    cu = wl.cu_seqlens()
+    B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, wl.n_heads, wl.head_dim)
+    y = empty((T, D), "bf16")
+    B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], o, db.d["txt"], mod, y, db.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_ref)
+
+
+def test_block_output_may_alias_input():
+    wl = SMALL_PACKED
+    log("case y aliases x")
+    db = DeviceBlock(wl)
+    y_ref = db.forward()
+    x = db.d["x"].clone()
+    db.forward(x=x, y=x)
+    torch.cuda.synchronize()
+    assert torch.equal(x, y_ref)
+
+
+@pytest.mark.parametrize("name", ["tiny_image_fp32", "small_packed_bf16"])
+def test_block_zero_gates_identity(name):
+    """gate_sa = gate_ff = 0 and W_co = b_co = 0 give y == x bitwise."""
+    wl = SMALL_PACKED if name == "small_packed_bf16" else synth.get_workload(name)
+    log(f"case zero-gate identity {name}")
+    inp = synth.generate_block_inputs(wl)
+    D = wl.hidden
+    for c in (2, 5):
+        inp["w_ada"][c * D:(c + 1) * D] = 0
+        inp["b_ada"][c * D:(c + 1) * D] = 0
+    inp["w_co"][:] = 0
+    inp["b_co"][:] = 0
+    db = DeviceBlock(wl, inputs=inp)
+    y = db.forward()
+    torch.cuda.synchronize()
+    assert torch.equal(y, db.d["x"])
+
+
+def test_block_permutation_equivariance_without_rope():
+    base = SMALL_PACKED
+    wl = Workload(**{**base.__dict__, "name": "small_packed_norope", "rope_sections": (0, 0, 0)})
+    log("case permutation equivariance")
+    db = DeviceBlock(wl)
+    y = host(db.forward())
+    rng = np.random.default_rng(7)
+    cu = wl.cu_seqlens()
+    perm = np.concatenate([cu[r] + rng.permutation(cu[r + 1] - cu[r]) for r in range(wl.n_req)])
+    xp = db.d["x"][torch.from_numpy(perm).cuda()].contiguous()
+    yp = host(db.forward(x=xp))
+    torch.cuda.synchronize()
+    check(yp, y[perm], "bf16", "permuted")
+
+
+def test_shard_rows_equal_full_rows():
+    """A sequence-parallel shard (pos_offset) gives the same pre-attention
+    rows as the full request (per-token steps), bitwise."""
+    wl = Workload(**{**SMALL_PACKED.__dict__, "name": "one_req", "grids": ((3, 9, 19),), "rows": (513,),
+                     "txt_len": 64})
+    log("case shard rows")
+    db = DeviceBlock(wl)
+    B = db.B
+    D = wl.hidden
+    mod = torch.empty((1, 6, D), dtype=torch.float32, device="cuda")
+    full = empty((513, 3 * D), "bf16")
+    B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, full, db.ws)
+    a, b = 171, 342
+    vls = B.Varlen([0, b - a], [0, 64], [(3, 9, 19)], [a])
+    shard = empty((b - a, 3 * D), "bf16")
+    xs = db.d["x"][a:b].contiguous()
+    ws = torch.empty(B.block_workspace_size(db.cfg, vls), dtype=torch.uint8, device="cuda")
+    B.block_pre_attention(db.cfg, db.w, vls, xs, db.d["t"], mod, shard, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(shard, full[a:b])

@@ -1,0 +1,248 @@
+"""Per-kernel parity of the HIP path against the CPU oracle, through the C ABI.
+
+Inputs are seeded (synth.draw); both sides read the same stored bits.  Sizes
+span several tiles with ragged tails, packed batches of several requests,
+single-row and empty requests."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import dit_block as O
+from gpu_util import require_gpu, dev, host, empty, check, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _cu(lengths):
+    return np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+
+
+def _req_of(cu):
+    return np.concatenate([np.full(cu[r + 1] - cu[r], r) for r in range(len(cu) - 1)]).astype(np.int64)
+
+
+# ------------------------------------------------------------------ LayerNorm
+
+
+@pytest.mark.parametrize("dtype,D,lengths", [
+    ("bf16", 3072, [5, 1000, 331]), ("bf16", 5120, [1, 257]), ("f32", 384, [64]), ("f32", 384, [3, 20, 41])])
+def test_adaln_modulate(dtype, D, lengths):
+    B = require_gpu()
+    log(f"case adaln_modulate {dtype} D={D} lengths={lengths}")
+    cu = _cu(lengths)
+    R, T = len(lengths), int(cu[-1])
+    x = synth.draw((T, D), (1, D, T), dtype)
+    mod = synth.draw((R, 6, D), (2, D, T), "f32", std=0.5)
+    out = empty((T, D), dtype)
+    mt = dev(mod)
+    B.adaln_modulate(dev(x), mt[:, 3], mt[:, 4], 6 * D, cu, 1e-6, out)
+    torch.cuda.synchronize()
+    req = _req_of(cu)
+    ref = O.modulate(O.layer_norm(O.decode(x), 1e-6), mod[req, 3].astype(np.float64), mod[req, 4].astype(np.float64))
+    check(host(out), ref, dtype, "adaln_modulate")
+
+
+@pytest.mark.parametrize("dtype,D,T", [("bf16", 5120, 777), ("f32", 384, 64)])
+def test_layer_norm_affine(dtype, D, T):
+    B = require_gpu()
+    log(f"case layer_norm_affine {dtype} D={D} T={T}")
+    x = synth.draw((T, D), (3, D), dtype)
+    g = synth.draw((D,), (4, D), dtype, mean=1.0, std=0.02)
+    b = synth.draw((D,), (5, D), dtype, std=0.02)
+    out = empty((T, D), dtype)
+    B.layer_norm_affine(dev(x), dev(g), dev(b), 1e-6, out)
+    torch.cuda.synchronize()
+    ref = O.layer_norm(O.decode(x), 1e-6) * O.decode(g) + O.decode(b)
+    check(host(out), ref, dtype, "layer_norm_affine")
+
+
+# ------------------------------------------------------------------ GEMM
+
+GEMM_CASES = [
+    ("bf16", 1000, 768, 1024, [1000]),       # ragged M, several tiles
+    ("bf16", 300, 264, 64, [100, 200]),       # N tail (not a multiple of 256), K = one tile
+    ("bf16", 4096 + 77, 512, 3072, [4096, 77]),
+    ("f32", 64, 1536, 384, [64]),
+    ("f32", 77, 768, 384, [30, 47]),
+]
+
+
+@pytest.mark.parametrize("dtype,M,N,K,lengths", GEMM_CASES)
+@pytest.mark.parametrize("epi", [0, 1, 2, 3])
+def test_linear(dtype, M, N, K, lengths, epi):
+    B = require_gpu()
+    log(f"case linear {dtype} M={M} N={N} K={K} epi={epi} lengths={lengths}")
+    cu = _cu(lengths)
+    a = synth.draw((M, K), (10, M, N, K), dtype)
+    w = synth.draw((N, K), (11, M, N, K), dtype, std=0.02)
+    b = synth.draw((N,), (12, M, N, K), dtype, std=0.02)
+    res = synth.draw((M, N), (13, M, N, K), dtype)
+    gate = synth.draw((len(lengths), 2 * N), (14, M, N, K), "f32", std=0.7)
+    out = empty((M, N), dtype)
+    gt = dev(gate)
+    B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
+             gate=gt[:, N:] if epi == 3 else None, gate_stride=2 * N, cu_seqlens=cu if epi == 3 else None)
+    torch.cuda.synchronize()
+    z = O.linear(O.decode(a), O.decode(w), O.decode(b))
+    if epi == 1:
+        z = O.gelu_tanh(z)
+    elif epi == 2:
+        z = O.decode(res) + z
+    elif epi == 3:
+        z = O.decode(res) + gate[_req_of(cu), N:].astype(np.float64) * z
+    check(host(out), z, dtype, f"linear epi={epi}")
+
+
+def test_linear_inplace_residual():
+    """res == out (the block updates x1 in place)."""
+    B = require_gpu()
+    log("case linear in-place residual bf16 M=515 N=512 K=256")
+    M, N, K = 515, 512, 256
+    a = synth.draw((M, K), (15,), "bf16")
+    w = synth.draw((N, K), (16,), "bf16", std=0.05)
+    r = synth.draw((M, N), (17,), "bf16")
+    out = dev(r)
+    B.linear(dev(a), dev(w), None, out, epi=2, res=out)
+    torch.cuda.synchronize()
+    check(host(out), O.decode(r) + O.linear(O.decode(a), O.decode(w), None), "bf16", "in-place residual")
+
+
+# ------------------------------------------------------------ RMSNorm + rotary
+
+
+@pytest.mark.parametrize("dtype,H,d,sections,lengths,grids,offsets", [
+    ("bf16", 4, 128, (44, 42, 42), [700, 500], [(3, 10, 30), (2, 20, 20)], [0, 100]),
+    ("bf16", 3, 128, (0, 64, 64), [1, 300], [(1, 4, 4), (1, 20, 16)], [5, 19]),
+    ("f32", 6, 64, (0, 32, 32), [64], [(1, 8, 8)], [0]),
+])
+def test_qk_norm_rope(dtype, H, d, sections, lengths, grids, offsets):
+    B = require_gpu()
+    log(f"case qk_norm_rope {dtype} H={H} d={d} sections={sections} lengths={lengths}")
+    cu = _cu(lengths)
+    T, D = int(cu[-1]), H * d
+    qkv = synth.draw((T, 3 * D), (20, H, T), dtype)
+    gq = synth.draw((d,), (21, H), dtype, mean=1.0, std=0.1)
+    gk = synth.draw((d,), (22, H), dtype, mean=1.0, std=0.1)
+    t = dev(qkv)
+    vl = B.Varlen(cu, None, grids, offsets)
+    B.qk_norm_rope(t[:, :D], t[:, D:2 * D], H, d, dev(gq), dev(gk), 1e-6, sections, 10000.0, vl)
+    torch.cuda.synchronize()
+    g = host(t)
+    src = O.decode(qkv)
+    cfg = O.BlockConfig(hidden=D, n_heads=H, head_dim=d, mlp_hidden=4, freq_dim=4, rope_sections=sections)
+    ovl = O.Varlen(list(cu), [0] * len(cu), grids, offsets)
+    rq = O.rope_for_rows(O.rms_norm_heads(src[:, :D], O.decode(gq), H, d, 1e-6), cfg, ovl)
+    rk = O.rope_for_rows(O.rms_norm_heads(src[:, D:2 * D], O.decode(gk), H, d, 1e-6), cfg, ovl)
+    check(g[:, :D], rq, dtype, "q")
+    check(g[:, D:2 * D], rk, dtype, "k")
+    assert np.array_equal(g[:, 2 * D:], src[:, 2 * D:]), "v must be untouched"
+
+
+def test_rms_norm_only():
+    """RMSNorm without rotary and without a second tensor (cross-attention query)."""
+    B = require_gpu()
+    log("case rms_norm only bf16 H=5 T=333")
+    H, d, T = 5, 128, 333
+    q = synth.draw((T, 2 * H * d), (23,), "bf16")
+    g = synth.draw((d,), (24,), "bf16", mean=1.0, std=0.1)
+    t = dev(q)
+    B.qk_norm_rope(t[:, :H * d], None, H, d, dev(g), None, 1e-6)
+    torch.cuda.synchronize()
+    out = host(t)
+    check(out[:, :H * d], O.rms_norm_heads(O.decode(q)[:, :H * d], O.decode(g), H, d, 1e-6), "bf16", "rms only")
+    assert np.array_equal(out[:, H * d:], O.decode(q)[:, H * d:])
+
+
+# ------------------------------------------------------------------ attention
+
+ATTN_CASES = [
+    # dtype, heads, d, query lengths, key lengths (None = self-attention)
+    ("bf16", 3, 128, [1, 255, 256, 700, 64], None),
+    ("bf16", 2, 128, [100, 0, 513], [77, 40, 512]),
+    ("bf16", 1, 128, [2048], None),
+    ("f32", 6, 64, [64], None),
+    ("f32", 6, 64, [64], [77]),
+    ("f32", 2, 128, [5, 30], [7, 1]),
+]
+
+
+@pytest.mark.parametrize("dtype,H,d,lq,lk", ATTN_CASES)
+def test_attention_varlen(dtype, H, d, lq, lk):
+    B = require_gpu()
+    log(f"case attention {dtype} H={H} d={d} lq={lq} lk={lk}")
+    cu_q = _cu(lq)
+    cu_k = cu_q if lk is None else _cu(lk)
+    Tq, Tk, W = int(cu_q[-1]), int(cu_k[-1]), H * d
+    # q, k, v as strided views of packed buffers, like the block's qkv
+    qb = synth.draw((Tq, 3 * W), (30, H, Tq, Tk), dtype)
+    kvb = synth.draw((Tk, 2 * W), (31, H, Tq, Tk), dtype)
+    qt, kvt = dev(qb), dev(kvb)
+    out = empty((Tq, W), dtype)
+    B.attention_varlen(qt[:, :W], kvt[:, :W], kvt[:, W:], out, cu_q, cu_k, H, d)
+    torch.cuda.synchronize()
+    ref = O.attention_varlen(O.decode(qb)[:, :W], O.decode(kvb)[:, :W], O.decode(kvb)[:, W:], cu_q, cu_k, H, d)
+    check(host(out), ref, dtype, "attention")
+
+
+def test_attention_varlen_no_leakage():
+    """A packed batch equals each request run alone (bitwise: same tiles)."""
+    B = require_gpu()
+    log("case attention packed vs alone bf16")
+    H, d, lens = 2, 128, [300, 129, 600]
+    cu = _cu(lens)
+    W = H * d
+    qkv = dev(synth.draw((int(cu[-1]), 3 * W), (32,), "bf16"))
+    packed = empty((int(cu[-1]), W), "bf16")
+    B.attention_varlen(qkv[:, :W], qkv[:, W:2 * W], qkv[:, 2 * W:], packed, cu, cu, H, d)
+    for r in range(len(lens)):
+        a, b = int(cu[r]), int(cu[r + 1])
+        one = empty((b - a, W), "bf16")
+        sub = qkv[a:b]
+        B.attention_varlen(sub[:, :W], sub[:, W:2 * W], sub[:, 2 * W:], one, [0, b - a], [0, b - a], H, d)
+        torch.cuda.synchronize()
+        assert torch.equal(one, packed[a:b]), f"request {r} differs when packed"
+
+
+# ------------------------------------------------------------ gated residual
+
+
+@pytest.mark.parametrize("dtype,D,lengths", [("bf16", 3072, [10, 500, 3]), ("f32", 384, [64])])
+def test_gated_residual(dtype, D, lengths):
+    B = require_gpu()
+    log(f"case gated_residual {dtype} D={D} lengths={lengths}")
+    cu = _cu(lengths)
+    T, R = int(cu[-1]), len(lengths)
+    x = synth.draw((T, D), (40, D), dtype)
+    z = synth.draw((T, D), (41, D), dtype)
+    b = synth.draw((D,), (42, D), dtype, std=0.02)
+    g = synth.draw((R, 6 * D), (43, D), "f32", std=0.7)
+    out = empty((T, D), dtype)
+    gt = dev(g)
+    B.gated_residual(dev(x), dev(z), dev(b), gt[:, 2 * D:], 6 * D, cu, out)
+    torch.cuda.synchronize()
+    ref = O.decode(x) + g[_req_of(cu), 2 * D:3 * D].astype(np.float64) * (O.decode(z) + O.decode(b))
+    check(host(out), ref, dtype, "gated_residual")
+
+
+# ------------------------------------------------------------ conditioning
+
+
+@pytest.mark.parametrize("name,n_req", [("tiny_image_fp32", 1), ("tiny_image_fp32", 3), ("image_1024", 3)])
+def test_timestep_modulation(name, n_req):
+    B = require_gpu()
+    log(f"case timestep_modulation {name} n_req={n_req}")
+    wl = synth.get_workload(name)
+    names = ["w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada"]
+    inp = synth.generate_block_inputs(wl, names)
+    t = synth.draw((n_req,), (50, n_req), "f32", dist="uniform", lo=0.0, hi=1000.0)
+    d = {k: dev(v) for k, v in inp.items()}
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    cfg = B.BlockConfig(wl.hidden, wl.n_heads, wl.head_dim, wl.mlp_hidden, wl.freq_dim, wl.rope_sections, tdt)
+    mod = torch.empty((n_req, 6, wl.hidden), dtype=torch.float32, device="cuda")
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    B.timestep_modulation(cfg, B.make_weights(d), dev(t), mod, ws)
+    torch.cuda.synchronize()
+    ow = {k: O.decode(v) for k, v in inp.items()}
+    ref = O.conditioning(t.astype(np.float64), wl.freq_dim, ow)
+    check(host(mod), ref, "f32" if wl.dtype == "f32" else "bf16", "modulation")
