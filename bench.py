@@ -1,0 +1,249 @@
+"""Throughput of one DiT block forward on one MI355X.
+
+One step = one pass of the whole hot path over one batch: timestep
+conditioning, modulated LayerNorm, QKV projection, QK-RMSNorm + rotary,
+self-attention, gated output projection, cross-attention to text, gated GELU
+MLP.  The default workload is the 720p video block (75,600 latent tokens,
+D = 5120, 40 heads of 128, MLP 13824, 512 text tokens), bf16 with fp32
+accumulation, seeded synthetic inputs resident in HBM before timing starts.
+
+The timed step runs the block through the library's seam entry points
+(pre-attention -> attention -> post-attention; bitwise equal to
+dit_block_forward) so that HIP events on the library's stream bracket the
+self-attention kernel, the dominant one, inside the timed region.  The
+dit_block_forward entry point is timed as well.
+
+Prints ONE JSON line (rank 0).  --gpus > 1 is refused: this build runs on one
+GPU.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DiT block fwd ms + TFLOP/s (% bf16 MFMA peak) at 32K/75K video tokens"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "attn_fwd_bf16.video_720p.traffic.txt")
+ATTN_SOURCE = os.path.join(ROOT, "paper_2606_13501_amd", "csrc", "attention.hip")
+
+
+def block_flops(wl):
+    """Algorithmic flops of one block (2 per multiply-add; attention 4 n^2 H d
+    non-causal for self, 4 n L H d for cross)."""
+    D, F, Dff, d = wl.hidden, wl.freq_dim, wl.mlp_hidden, wl.head_dim
+    T, R, Lt = wl.n_rows, wl.n_req, wl.n_txt
+    a_rows = wl.attn_rows if wl.attn_rows is not None else wl.rows
+    a_heads = wl.attn_heads if wl.attn_heads is not None else wl.n_heads
+    f = {
+        "cond": 2.0 * R * (D * F + D * D + 6 * D * D),
+        "gemm": 2.0 * T * D * (3 * D + D + D + D + 2 * Dff) + 2.0 * Lt * D * 2 * D,
+        "self_attn": sum(4.0 * n * n * a_heads * d for n in a_rows),
+        "cross_attn": sum(4.0 * n * wl.txt_len * wl.n_heads * d for n in wl.rows),
+    }
+    f["total"] = sum(f.values())
+    return f
+
+
+def read_traffic():
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, or None when it is missing or was taken on another kernel source."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    kv = {}
+    for line in open(PROFILE_TRAFFIC):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    src_sha = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()[:16]
+    if kv.get("kernel_source_sha256_16") != src_sha:
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, target_s=12.0):
+    """The oracle (float64 NumPy) on a bounded sample of the same workload:
+    every per-token step for n sampled query rows of the request, with their
+    self-attention over all of the request's keys (seeded K and V, all heads)
+    and cross-attention over its text.  Reported in TFLOP/s of the sample's
+    algorithmic flops."""
+    import numpy as np
+    import synth
+    from oracle import dit_block as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    inp = synth.generate_block_inputs(wl)
+    w = {k: O.decode(v) for k, v in inp.items()}
+    del inp
+    att = synth.generate_attention_inputs(wl)
+    D, H, d = wl.hidden, wl.n_heads, wl.head_dim
+    K = O.decode(att["k"]).reshape(-1, H * d)
+    V = O.decode(att["v"]).reshape(-1, H * d)
+    del att
+    cfg = O.config_from_workload(wl)
+    n_all = wl.rows[0]
+
+    def run(n):
+        rows = np.linspace(0, n_all - 1, n).astype(np.int64)
+        t0 = time.perf_counter()
+        mod = O.conditioning(w["t"], cfg.freq_dim, w)
+        # per-token pre-attention steps on the sampled rows: each row is its own
+        # one-row request at its grid position, all sharing the request's modulation
+        rows_vl = O.Varlen(list(range(n + 1)), [0] * (n + 1), [wl.grids[0]] * n, [int(r) for r in rows])
+        q, _, _ = O.pre_attention(cfg, rows_vl, w["x"][rows], w, np.broadcast_to(mod, (n,) + mod.shape[1:]))
+        sub = O.Varlen([0, n], [0, wl.txt_len], [wl.grids[0]])
+        o = O.attention_varlen(q, K, V, [0, n], [0, n_all], H, d)
+        O.post_attention(cfg, sub, w["x"][rows], o, w["txt"], w, mod)
+        dt = time.perf_counter() - t0
+        Dff = wl.mlp_hidden
+        fl = n * (2.0 * D * (3 * D + 3 * D + 2 * Dff) + 4.0 * n_all * H * d + 4.0 * wl.txt_len * H * d) \
+            + 2.0 * wl.txt_len * D * 2 * D + 2.0 * (D * wl.freq_dim + 7 * D * D)
+        return dt, fl
+
+    dt, fl = run(16)
+    n = int(min(4096, max(16, 16 * target_s / max(dt, 1e-3))))
+    dt, fl = run(n)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"{wl.name}: all block steps for {n} evenly spaced query rows of the "
+                       f"{n_all}-token request (self-attention of those rows over all {n_all} keys, "
+                       f"{H} heads, seeded K/V; cross-attention over {wl.txt_len} text tokens); "
+                       f"float64 NumPy, {dt:.1f} s")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="video_720p")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              f"multi-GPU sharding is designed but not built", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    import paper_2606_13501_amd.binding as B
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    torch.cuda.set_device(0)
+    wl = synth.get_workload(args.workload)
+    t0 = time.time()
+    inp = synth.generate_block_inputs(wl)
+    print(f"[bench] generated {wl.name} inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    def dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    d = {k: dev(v) for k, v in inp.items()}
+    del inp
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    cfg = B.BlockConfig(wl.hidden, wl.n_heads, wl.head_dim, wl.mlp_hidden, wl.freq_dim, wl.rope_sections, tdt)
+    w = B.make_weights(d)
+    vl = B.Varlen(wl.cu_seqlens(), wl.cu_txt(), list(wl.grids))
+    ws = torch.empty(B.block_workspace_size(cfg, vl), dtype=torch.uint8, device="cuda")
+    T, D, H, hd = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
+    y = torch.empty_like(d["x"])
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    qkv = torch.empty((T, 3 * D), dtype=tdt, device="cuda")
+    o = torch.empty((T, D), dtype=tdt, device="cuda")
+    cu = wl.cu_seqlens()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        B.block_pre_attention(cfg, w, vl, d["x"], d["t"], mod, qkv, ws)
+        if ev is not None:
+            ev[0].record(stream)
+        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
+        if ev is not None:
+            ev[1].record(stream)
+        B.block_post_attention(cfg, w, vl, d["x"], o, d["txt"], mod, y, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    attn_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+
+    # the single-call entry point, same work
+    fstart, fstop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    fstart.record(stream)
+    for _ in range(args.steps):
+        B.block_forward(cfg, w, vl, d["x"], d["t"], d["txt"], y, ws)
+    fstop.record(stream)
+    torch.cuda.synchronize()
+    fwd_ms = fstart.elapsed_time(fstop) / args.steps
+
+    fl = block_flops(wl)
+    tflops = fl["total"] / (ms * 1e-3) / 1e12
+    attn_flops = fl["self_attn"]
+    attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
+    traffic = read_traffic()
+    out = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded; shapes of the paper's Wan2.2 720p request class, random-init weights)",
+        "config": {
+            "workload": wl.name, "tokens": T, "requests": wl.n_req, "hidden": D, "heads": H, "head_dim": hd,
+            "mlp_hidden": wl.mlp_hidden, "text_tokens": wl.n_txt, "rope_sections": list(wl.rope_sections),
+            "block_flops": fl["total"], "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
+            "ms_per_step_block_forward_entry": round(fwd_ms, 3),
+        },
+        "roofline": {
+            "kernel": "attn_fwd_bf16 (self-attention)",
+            "bound": "mfma",
+            "achieved": round(attn_tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "flops_per_launch": attn_flops,
+            "ms_per_launch": round(attn_ms, 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(wl)
+        print(f"[bench] cpu baseline took {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
