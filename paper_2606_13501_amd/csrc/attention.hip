@@ -16,6 +16,8 @@
 // for the PV product.
 //
 // fp32: one thread per (query row, head) with an exact online softmax.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -28,9 +30,16 @@ constexpr int BQ = 256;          // query rows per workgroup
 constexpr int BKV = 64;          // keys per LDS tile
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kKBytes = BKV * D * 2;     // 16 KiB
-constexpr int kVBytes = BKV * D * 2;     // 16 KiB
-constexpr int kStage = kKBytes + kVBytes;
+// K rows (one key, 256 B) are padded to a 272-byte pitch, so that fragment
+// reads of 8 or 16 consecutive rows hit distinct banks and every K fragment
+// address is a per-lane base plus an immediate.  V^T rows (one d, 64 keys =
+// 128 B) are unpadded; their 16-byte chunks are XOR-swizzled with
+// vt_swizzle(d), conflict-free both for the transposing writes and for the
+// fragment reads.
+constexpr int kKPitch = D * 2 + 16;
+constexpr int kVPitch = BKV * 2;
+constexpr int kKBytes = BKV * kKPitch;   // 17 KiB
+constexpr int kVBytes = D * kVPitch;     // 18 KiB
 constexpr int kXcds = 8;
 
 struct AttnWork {
@@ -48,6 +57,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
+__device__ __forceinline__ int vt_swizzle(int d) { return (d & 7) ^ ((d >> 3) & 3); }
+
 // swap bits 2 and 3 of a key index inside its 16-key group
 __device__ __forceinline__ int perm23(int x) {
   return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1);
@@ -57,7 +68,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
     float scale_log2, AttnWork work) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+  // K(j) in K slot j & 1, V(j) in V slot j & 1
+  __shared__ __attribute__((aligned(16))) char smem[2 * kKBytes + 2 * kVBytes];
+  char* const kslots = smem;
+  char* const vslots = smem + 2 * kKBytes;
 
   // ---- work item: XCD-contiguous numbering, requests longest first
   const int nb = gridDim.x;
@@ -90,22 +104,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + 16 * kk);
   }
 
-  // ---- global -> LDS staging
-  // K: 2 chunks of 16 B per thread: key = (tid >> 4) + 32 i, chunk c = tid & 15
+  // ---- global -> LDS staging (all 512 threads share every tile)
   // buffer resources are rebased at every tile so offsets stay small; loads
   // past the request's last key return zeros
   const bf16* k_head = K + (int64_t)k0 * ks + head * D;
   const bf16* v_head = V + (int64_t)k0 * vs + head * D;
+  // K: 2 chunks of 16 B per thread: key (tid >> 4) + 32 i, chunk tid & 15;
+  // key k is stored in row slot perm23(k) so that MFMA row fr reads slot fr
   const int kl_key = tid >> 4;
   const int kl_c = tid & 15;
   const int kl_voff = kl_key * (int)ks * 2 + kl_c * 16;
-  int kl_st[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int key = kl_key + 32 * i;
-    kl_st[i] = key * 256 + ((kl_c ^ perm23(key & 15)) << 4);
-  }
-  // V: keys 4 kg .. 4 kg + 3, d 4 dc .. 4 dc + 3 (8-byte loads), written as V^T
+  const int kl_st = perm23(kl_key) * kKPitch + kl_c * 16;   // + 32 kKPitch for i = 1
+  // V: keys 4 kg .. 4 kg + 3, d 4 dc .. 4 dc + 3 (8-byte loads; a wave reads
+  // two whole 256-byte key rows per load), written transposed as V^T
   const int vl_lo = tid & 1;
   const int vl_dc = (tid >> 1) & 31;
   const int vl_kg = 2 * (tid >> 6) + vl_lo;
@@ -113,33 +124,37 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   int vl_st[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    int d = 4 * vl_dc + e;
-    int c = vl_kg >> 1;
-    vl_st[e] = d * 128 + ((c ^ ((d ^ (d >> 3)) & 7)) << 4) + (vl_kg & 1) * 8;
+    const int d = 4 * vl_dc + e;
+    vl_st[e] = d * kVPitch + (((vl_kg >> 1) ^ vt_swizzle(d)) << 4) + (vl_kg & 1) * 8;
   }
 
   u32x4 kreg[2];
   u32x2 vreg[4];
-  auto gload = [&](int kt) {
+  auto gload_k = [&](int kt) {
     const int kb0 = kt * BKV;
-    const __amdgpu_buffer_rsrc_t k_rs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
-    const __amdgpu_buffer_rsrc_t v_rs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(k_rs, kl_voff, 32 * i * (int)ks * 2, 0);
+      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, kl_voff, 32 * i * (int)ks * 2, 0);
+  };
+  auto gload_v = [&](int kt) {
+    const int kb0 = kt * BKV;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      vreg[i] = __builtin_amdgcn_raw_buffer_load_b64(v_rs, vl_voff, i * (int)vs * 2, 0);
+      vreg[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, vl_voff, i * (int)vs * 2, 0);
     // keys past the request end: zero V so that P = 0 times V stays exact
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (kb0 + 4 * vl_kg + i >= n_k) vreg[i] = u32x2{0u, 0u};
   };
-  auto sstore = [&](int stage) {
-    char* kb = smem + stage * kStage;
-    char* vb = kb + kKBytes;
+  auto sstore_k = [&](int kt) {
+    char* kb = kslots + (kt & 1) * kKBytes;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st[i]) = kreg[i];
+    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st + 32 * i * kKPitch) = kreg[i];
+  };
+  auto sstore_v = [&](int kt) {
+    char* vb = vslots + (kt & 1) * kVBytes;
     // transpose 4 keys x 4 d: element (key i, d e) -> V^T[d e][key i]
     const uint16_t* vv = reinterpret_cast<const uint16_t*>(vreg);
 #pragma unroll
@@ -151,98 +166,129 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     }
   };
 
-  // ---- fragment read offsets
-  // K (A operand of S^T): key 32 kb + perm23(fr), chunk 2 kk + fh
-  const int kf_key = perm23(fr);
-  const int kf_base = kf_key * 256;
-  const int kf_sw = perm23(kf_key & 15);   // == fr & 15
-  // V^T (A operand of O^T): row d = 32 dblk + fr, chunk 4 kb + 2 s + fh
-  int vf_sw[4];   // (d ^ (d >> 3)) & 7 with d = 32 dblk + fr
+  // ---- fragment read offsets inside a slot
+  // K (A operand of S^T): slot 32 blk + fr (= key 32 blk + perm23(fr)), d 16 kk + 8 fh
+  const int koff = fr * kKPitch + fh * 16;             // + blk 32 kKPitch + kk 32
+  // V^T (A operand of O^T): row d = 32 dblk + fr, 16-byte chunk 2 (2 blk + hs) + fh
+  // (vt_swizzle(32 dblk + fr) == vt_swizzle(fr))
+  int voff[4];                                         // [2 blk + hs], + dblk 32 kVPitch
 #pragma unroll
-  for (int dblk = 0; dblk < 4; ++dblk) vf_sw[dblk] = (fr ^ (4 * dblk + (fr >> 3))) & 7;
+  for (int c4 = 0; c4 < 4; ++c4) voff[c4] = fr * kVPitch + (((2 * c4 + fh) ^ vt_swizzle(fr)) << 4);
+
+  const int n_tiles = (n_k + BKV - 1) / BKV;
+  const int n_full = n_k / BKV;
 
   f32x16 oacc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) oacc[i] = f32x16{};
-  float m_run = -INFINITY;   // running max of (score * scale_log2)
-  float l_run = 0.f;         // this lane's share of the running sum
+  f32x16 s[2];          // scores of the current tile: s[blk][4i + j] = S[q = fr][key 32 blk + perm23(8 i + 4 fh + j)]
+  bf16x8 pf[2][2];      // probabilities of the current tile, PV operand
+  float m_tile = 0.f;   // max of the current tile's scores of the lane's row (times scale_log2)
+  // Running max of (score * scale_log2) of the lane's query row.  It is only
+  // raised when a tile's max exceeds it by more than kLazy (log2 units), so
+  // that the O rescale is skipped for most tiles; probabilities are then
+  // bounded by 2^kLazy, harmless in fp32 and bf16.
+  constexpr float kLazy = 8.0f;
+  float m_run = -INFINITY;
+  float l_run = 0.f;    // this lane's share of the running sum
 
-  const int n_tiles = (n_k + BKV - 1) / BKV;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < n_tiles) gload(kt + 1);
-    const char* kb = smem + cur * kStage;
-    const char* vb = kb + kKBytes;
-
-    // S^T for 2 blocks of 32 keys: s[kb][4i + j] = S[q = fr][key 32 kb + 8 i + 4 fh + j]
-    // (key order inside a 32-key block: row rho of the MFMA is key perm23(rho))
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+  // S(j) = K(j) Q^T
+  auto mma_s = [&](int j) {
+    const char* kb = kslots + (j & 1) * kKBytes + koff;
+    s[0] = f32x16{};
+    s[1] = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      const int c = 2 * kk + fh;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + blk * 32 * 256 + kf_base + ((c ^ kf_sw) << 4));
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + blk * 32 * kKPitch + kk * 32);
         s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[blk], 0, 0, 0);
       }
     }
-
-    // mask keys past the request end (only the last tile can have them)
-    const int kbase = kt * BKV;
-    if (kbase + BKV > n_k) {
+  };
+  // O^T += V^T(j) P^T(j)
+  auto mma_pv = [&](int j) {
+    const char* vb = vslots + (j & 1) * kVBytes;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int hs = 0; hs < 2; ++hs)
+#pragma unroll
+        for (int dblk = 0; dblk < 4; ++dblk) {
+          bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + voff[2 * blk + hs] + dblk * 32 * kVPitch);
+          oacc[dblk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[blk][hs], oacc[dblk], 0, 0, 0);
+        }
+  };
+  // mask of the ragged last tile (masked == true), then the row max of S(j)
+  auto row_max = [&](int j, auto masked) {
+    if (decltype(masked)::value) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          int key = kbase + 32 * blk + perm23(8 * (v >> 2) + 4 * fh + (v & 3));
+          const int key = j * BKV + 32 * blk + perm23(8 * (v >> 2) + 4 * fh + (v & 3));
           if (key >= n_k) s[blk][v] = -INFINITY;
         }
     }
-
-    // online softmax for query row fr (the other half-wave holds the other keys)
-    float mx = -INFINITY;
+    // the lane's 32 scores, then the other half-wave's 32 (same row)
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
+    for (int v = 3; v < 15; v += 2) mx = fmaxf(fmaxf(mx, s[0][v]), s[0][v + 1]);
+    mx = fmaxf(mx, s[0][15]);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[blk][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * scale_log2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    for (int v = 0; v < 16; v += 2) mx = fmaxf(fmaxf(mx, s[1][v]), s[1][v + 1]);
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    m_tile = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+  };
+  // online softmax of S into P
+  auto softmax = [&]() {
+    if (__builtin_amdgcn_ballot_w64(m_tile > m_run + kLazy) != 0) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
+    }
     float psum = 0.f;
-    bf16x8 pf[2][2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale_log2, -m_new));
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale_log2, -m_run));
         psum += p;
         pf[blk][v >> 3][v & 7] = (bf16)p;
       }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
-
-    // O^T += V^T P^T: 4 d-blocks x (2 key blocks x 2 halves of 16 keys)
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int hs = 0; hs < 2; ++hs) {
-        const int c = 4 * blk + 2 * hs + fh;
-#pragma unroll
-        for (int dblk = 0; dblk < 4; ++dblk) {
-          const int d = 32 * dblk + fr;
-          bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + d * 128 + ((c ^ vf_sw[dblk]) << 4));
-          oacc[dblk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[blk][hs], oacc[dblk], 0, 0, 0);
-        }
-      }
-
-    if (kt + 1 < n_tiles) sstore(cur ^ 1);
+    l_run += psum;
+  };
+  // ---- main loop: tile j is computed from LDS slot j & 1 while tile j+1 is
+  // fetched into registers; full tiles inside the loop, the ragged last tile
+  // (with its key mask) after it, so that the loop body has a single path.
+  gload_k(0);
+  gload_v(0);
+  sstore_k(0);
+  sstore_v(0);
+  __syncthreads();
+  for (int j = 0; j < n_full; ++j) {
+    if (j + 1 < n_tiles) {
+      gload_k(j + 1);
+      gload_v(j + 1);
+    }
+    mma_s(j);
+    row_max(j, std::false_type{});
+    softmax();
+    mma_pv(j);
+    if (j + 1 < n_tiles) {
+      sstore_k(j + 1);
+      sstore_v(j + 1);
+    }
     __syncthreads();
+  }
+  if (n_full < n_tiles) {
+    mma_s(n_full);
+    row_max(n_full, std::true_type{});
+    softmax();
+    mma_pv(n_full);
   }
 
   // ---- normalise and store: oacc[dblk][4i + j] = O[q = fr][d = 32 dblk + 8 i + 4 fh + j]
