@@ -39,6 +39,7 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kKPitch = D * 2 + 16;
 constexpr int kVPitch = BKV * 2;
 constexpr int kKBytes = BKV * kKPitch;   // 17 KiB
+constexpr int kVSlots = 3;               // V^T tiles live one step longer than K tiles
 constexpr int kVBytes = D * kVPitch;     // 18 KiB
 constexpr int kXcds = 8;
 
@@ -68,8 +69,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
     float scale_log2, AttnWork work) {
-  // K(j) in K slot j & 1, V(j) in V slot j & 1
-  __shared__ __attribute__((aligned(16))) char smem[2 * kKBytes + 2 * kVBytes];
+  // K(j) in K slot j & 1, V(j) in V slot j % 3
+  __shared__ __attribute__((aligned(16))) char smem[2 * kKBytes + kVSlots * kVBytes];
   char* const kslots = smem;
   char* const vslots = smem + 2 * kKBytes;
 
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
   const int fr = lane & 31;
   const int fh = lane >> 5;
 
@@ -128,35 +129,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     vl_st[e] = d * kVPitch + (((vl_kg >> 1) ^ vt_swizzle(d)) << 4) + (vl_kg & 1) * 8;
   }
 
-  u32x4 kreg[2];
-  u32x2 vreg[4];
-  auto gload_k = [&](int kt) {
+  // two register staging sets: the loads of tile t go to set t & 1, two
+  // steps before the tile is read from LDS
+  u32x4 kreg[2][2];
+  u32x2 vreg[2][4];
+  auto gload = [&](int kt, auto set) {
+    constexpr int S = decltype(set)::value;
     const int kb0 = kt * BKV;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
+    const __amdgpu_buffer_rsrc_t krs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, kl_voff, 32 * i * (int)ks * 2, 0);
-  };
-  auto gload_v = [&](int kt) {
-    const int kb0 = kt * BKV;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
+      kreg[S][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, kl_voff, 32 * i * (int)ks * 2, 0);
+    // keys past the request end lie past the end of the buffer range and load
+    // as zeros, so P = 0 times V stays exact (no select on the loaded value,
+    // which would wait for the load right here)
+    const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      vreg[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, vl_voff, i * (int)vs * 2, 0);
-    // keys past the request end: zero V so that P = 0 times V stays exact
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (kb0 + 4 * vl_kg + i >= n_k) vreg[i] = u32x2{0u, 0u};
+      vreg[S][i] = __builtin_amdgcn_raw_buffer_load_b64(vrs, vl_voff, i * (int)vs * 2, 0);
   };
-  auto sstore_k = [&](int kt) {
+  auto sstore = [&](int kt, auto set) {
+    constexpr int S = decltype(set)::value;
     char* kb = kslots + (kt & 1) * kKBytes;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st + 32 * i * kKPitch) = kreg[i];
-  };
-  auto sstore_v = [&](int kt) {
-    char* vb = vslots + (kt & 1) * kVBytes;
+    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st + 32 * i * kKPitch) = kreg[S][i];
+    char* vb = vslots + (kt % kVSlots) * kVBytes;
     // transpose 4 keys x 4 d: element (key i, d e) -> V^T[d e][key i]
-    const uint16_t* vv = reinterpret_cast<const uint16_t*>(vreg);
+    const uint16_t* vv = reinterpret_cast<const uint16_t*>(vreg[S]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       u32x2 t;
@@ -192,23 +191,34 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   float m_run = -INFINITY;
   float l_run = 0.f;    // this lane's share of the running sum
 
-  // S(j) = K(j) Q^T
+  // S(j) = K(j) Q^T, as four independent MFMA chains (even and odd d-steps of
+  // each 32-key block) summed at the end, so that no MFMA waits on the result
+  // of the one issued just before it
   auto mma_s = [&](int j) {
     const char* kb = kslots + (j & 1) * kKBytes + koff;
-    s[0] = f32x16{};
-    s[1] = f32x16{};
+    f32x16 s2[2][2];
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
         bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + blk * 32 * kKPitch + kk * 32);
-        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[blk], 0, 0, 0);
+        s2[blk][kk & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], kk < 2 ? f32x16{} : s2[blk][kk & 1], 0, 0, 0);
       }
     }
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) s[blk] = s2[blk][0] + s2[blk][1];
+    // keep four fragment reads in flight ahead of the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
   };
   // O^T += V^T(j) P^T(j)
   auto mma_pv = [&](int j) {
-    const char* vb = vslots + (j & 1) * kVBytes;
+    const char* vb = vslots + (j % kVSlots) * kVBytes;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
@@ -218,6 +228,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
           bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + voff[2 * blk + hs] + dblk * 32 * kVPitch);
           oacc[dblk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[blk][hs], oacc[dblk], 0, 0, 0);
         }
+    // keep four fragment reads in flight ahead of the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
   };
   // mask of the ragged last tile (masked == true), then the row max of S(j)
   auto row_max = [&](int j, auto masked) {
@@ -261,29 +279,48 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
       }
     l_run += psum;
   };
-  // ---- main loop: tile j is computed from LDS slot j & 1 while tile j+1 is
-  // fetched into registers; full tiles inside the loop, the ragged last tile
-  // (with its key mask) after it, so that the loop body has a single path.
-  gload_k(0);
-  gload_v(0);
-  sstore_k(0);
-  sstore_v(0);
+  // ---- main loop.  Step j computes tile j from LDS, issues the loads of
+  // tile j+2 (register set j & 1) at its start and stores tile j+1 (loaded
+  // one step earlier, set (j+1) & 1) to LDS before its barrier, so every load
+  // has two steps to arrive.  Full tiles inside the loop (unrolled by two for
+  // the register sets), the ragged last tile (with its key mask) after it.
+  // Waves 0-3 run S(j), softmax(j), PV(j) between two barriers.  Waves 4-7
+  // run the same sequence but take the barrier before PV(j), which they
+  // compute at the start of the next step: the two waves sharing a SIMD are
+  // then half a step apart, one on the matrix core while the other runs its
+  // softmax.  V(j) is read until the step after j, hence three V slots.
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  gload(0, S0{});
+  sstore(0, S0{});
+  if (n_tiles > 1) gload(1, S1{});
+  // every load issued so far (Q fragments included) has completed: without
+  // this the waits for the Q loads land inside the loop, where they would
+  // also wait for each step's K and V prefetch
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
-  for (int j = 0; j < n_full; ++j) {
-    if (j + 1 < n_tiles) {
-      gload_k(j + 1);
-      gload_v(j + 1);
-    }
+  const bool lead = wave < kWaves / 2;
+  auto step_full = [&](int j, auto set) {
+    constexpr int S = decltype(set)::value;
+    if (j + 2 < n_tiles) gload(j + 2, std::integral_constant<int, S>{});
+    if (!lead && j > 0) mma_pv(j - 1);
     mma_s(j);
     row_max(j, std::false_type{});
     softmax();
-    mma_pv(j);
-    if (j + 1 < n_tiles) {
-      sstore_k(j + 1);
-      sstore_v(j + 1);
-    }
+    if (lead) mma_pv(j);
+    if (j + 1 < n_tiles) sstore(j + 1, std::integral_constant<int, 1 - S>{});
     __syncthreads();
+  };
+  int j = 0;
+  for (; j + 2 <= n_full; j += 2) {
+    step_full(j, S0{});
+    step_full(j + 1, S1{});
   }
+  if (j < n_full) {
+    step_full(j, S0{});
+    ++j;
+  }
+  if (!lead && n_full > 0) mma_pv(n_full - 1);
   if (n_full < n_tiles) {
     mma_s(n_full);
     row_max(n_full, std::true_type{});
