@@ -121,6 +121,31 @@ def cpu_baseline(wl, target_s=12.0):
                        f"float64 NumPy, {dt:.1f} s")}
 
 
+def profile_kernel(args, wl):
+    """One kernel alone, args.steps times, for counter collection."""
+    import torch
+    import paper_2606_13501_amd.binding as B
+    if args.profile_kernel == "copy":
+        n = 1 << 29                                  # 2^29 two-byte elements = 1 GiB
+        a = torch.empty(n, dtype=torch.float16, device="cuda").fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(args.steps):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n}), flush=True)
+        return
+    T, D, H, hd = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
+    g = torch.Generator(device="cuda")
+    g.manual_seed(13501)
+    qkv = torch.randn((T, 3 * D), generator=g, device="cuda").to(torch.bfloat16)
+    o = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+    cu = wl.cu_seqlens()
+    for _ in range(args.steps):
+        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile": "attention", "workload": wl.name, "launches": args.steps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,6 +153,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="video_720p")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-kernel", choices=["attention", "copy"], default=None,
+                    help="run only one kernel (for rocprofv3 counter passes) and exit: the block's "
+                         "self-attention at the workload's shape, or a plain 1 GiB device copy used to "
+                         "calibrate the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -145,6 +174,9 @@ def main():
     B.lib()
     torch.cuda.set_device(0)
     wl = synth.get_workload(args.workload)
+    if args.profile_kernel:
+        profile_kernel(args, wl)
+        return
     t0 = time.time()
     inp = synth.generate_block_inputs(wl)
     print(f"[bench] generated {wl.name} inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)

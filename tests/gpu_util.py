@@ -93,3 +93,34 @@ class DeviceBlock:
 
     def oracle_weights(self):
         return {k: O.decode(v) for k, v in self.inp.items()}
+
+
+# ---------------------------------------------------------------- sampled rows
+
+
+def oracle_pre_rows(wl, w, mod, rows):
+    """Oracle pre-attention outputs (q, k, v) of the given global rows: each
+    row is evaluated as its own one-row request at its grid position."""
+    cfg = O.config_from_workload(wl)
+    cu = wl.cu_seqlens()
+    req = np.searchsorted(np.asarray(cu), rows, side="right") - 1
+    vl = O.Varlen(list(range(len(rows) + 1)), [0] * (len(rows) + 1), [wl.grids[r] for r in req],
+                  [int(rows[i] - cu[req[i]]) for i in range(len(rows))])
+    return O.pre_attention(cfg, vl, w["x"][rows], w, mod[req])
+
+
+def oracle_post_rows(wl, w, mod, o, rows):
+    """Oracle post-attention outputs of the given global rows (attention
+    output ``o`` indexed by global row), request by request with its text."""
+    cfg = O.config_from_workload(wl)
+    cu = wl.cu_seqlens()
+    cut = wl.cu_txt()
+    out = np.empty((len(rows), wl.hidden))
+    for r in range(wl.n_req):
+        m = np.nonzero((rows >= cu[r]) & (rows < cu[r + 1]))[0]
+        if len(m) == 0:
+            continue
+        vl = O.Varlen([0, len(m)], [0, cut[r + 1] - cut[r]], [wl.grids[r]])
+        out[m] = O.post_attention(cfg, vl, w["x"][rows[m]], o[rows[m]], w["txt"][cut[r]:cut[r + 1]], w,
+                                  mod[r:r + 1])
+    return out

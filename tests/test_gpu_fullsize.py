@@ -1,0 +1,99 @@
+"""Parity at full size: the 480p and 720p video blocks (32,760 and 75,600
+tokens) and the packed sequence-parallel share (four requests, 5 attention
+heads over 121,672 rows), in the launch configuration the benchmark times.
+
+The GPU computes every row; the oracle computes a seeded sample of rows
+(first and last row of every request, frame boundaries, random rows) from the
+same inputs.  Self-attention stages use seeded q, k, v; the whole block is
+compared with expected rows written by tests/golden/make_block_golden.py."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import dit_block as O
+from gpu_util import DeviceBlock, require_gpu, dev, host, empty, check, log, oracle_pre_rows, oracle_post_rows
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.mark.parametrize("name", ["video_720p", "video_480p", "packed_sp8_share"])
+def test_self_attention_full_size(name):
+    B = require_gpu()
+    wl = synth.get_workload(name)
+    H = wl.attn_heads or wl.n_heads
+    d = wl.head_dim
+    W = H * d
+    log(f"case full-size self-attention {name}: rows {wl.cu_attn()[-1]} heads {H}")
+    att = synth.generate_attention_inputs(wl)
+    T = att["q"].shape[0]
+    qkv = np.empty((T, 3 * W), dtype=np.uint16)   # packed like the block's qkv buffer
+    qkv[:, :W] = att["q"].reshape(T, W)
+    qkv[:, W:2 * W] = att["k"].reshape(T, W)
+    qkv[:, 2 * W:] = att["v"].reshape(T, W)
+    t = dev(qkv)
+    o = empty((T, W), "bf16")
+    cu = wl.cu_attn()
+    B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], o, cu, cu, H, d)
+    torch.cuda.synchronize()
+    rows = synth.generate_sampled_rows(wl, 24, sample_id=3, attn=True)
+    g = host(o[torch.from_numpy(rows).cuda()])
+    del t, o
+    ref = O.attention_varlen(O.decode(qkv[:, :W]), O.decode(qkv[:, W:2 * W]), O.decode(qkv[:, 2 * W:]), cu, cu, H, d,
+                             q_rows=rows)
+    check(g, ref, "bf16", f"{name} self-attention ({len(rows)} sampled rows)")
+
+
+@pytest.mark.parametrize("name", ["video_720p", "packed_sp8_share"])
+def test_pre_post_attention_full_size(name):
+    wl = synth.get_workload(name)
+    log(f"case full-size pre/post attention {name}: rows {wl.n_rows}")
+    db = DeviceBlock(wl)
+    B = db.B
+    T, D = wl.n_rows, wl.hidden
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    qkv = empty((T, 3 * D), "bf16")
+    B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, qkv, db.ws)
+    o_in = synth.generate_attention_inputs(wl)["o"]
+    y = empty((T, D), "bf16")
+    B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], dev(o_in), db.d["txt"], mod, y, db.ws)
+    torch.cuda.synchronize()
+    rows = synth.generate_sampled_rows(wl, 24, sample_id=4)
+    idx = torch.from_numpy(rows).cuda()
+    g_qkv = host(qkv[idx])
+    g_y = host(y[idx])
+    g_mod = host(mod)
+    del qkv, y
+    w = db.oracle_weights()
+    ref_mod = O.conditioning(w["t"], wl.freq_dim, w)
+    check(g_mod, ref_mod, "bf16", f"{name} modulation")
+    q, k, v = oracle_pre_rows(wl, w, ref_mod, rows)
+    check(g_qkv[:, :D], q, "bf16", f"{name} q")
+    check(g_qkv[:, D:2 * D], k, "bf16", f"{name} k")
+    check(g_qkv[:, 2 * D:], v, "bf16", f"{name} v")
+    ref_y = oracle_post_rows(wl, w, ref_mod, O.decode(o_in), rows)
+    x = w["x"][rows]
+    check(g_y, ref_y, "bf16", f"{name} post-attention y")
+    check(g_y - x, ref_y - x, "bf16", f"{name} post-attention y - x")
+
+
+@pytest.mark.parametrize("name", ["video_480p", "video_720p"])
+def test_block_full_size_vs_golden(name):
+    path = os.path.join(GOLDEN, f"block_{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"{path} not generated")
+    wl = synth.get_workload(name)
+    log(f"case full-size block {name}: rows {wl.n_rows}")
+    gold = np.load(path)
+    rows, ref = gold["rows"], gold["y"].astype(np.float64)
+    db = DeviceBlock(wl)
+    y = db.forward()
+    torch.cuda.synchronize()
+    g = host(y[torch.from_numpy(rows).cuda()])
+    x = O.decode(db.inp["x"][rows])
+    check(g, ref, "bf16", f"{name} block y ({len(rows)} sampled rows)")
+    check(g - x, ref - x, "bf16", f"{name} block y - x")
