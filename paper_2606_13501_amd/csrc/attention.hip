@@ -1,19 +1,33 @@
 // Scaled dot-product attention over a packed batch, non-causal (the denoising
 // step attends bidirectionally over the whole latent sequence).
 //
-// bf16, head_dim 128: flash-style kernel for gfx950.  One 512-thread workgroup
-// (8 waves, 2 per SIMD) owns 256 query rows of one (request, head); each wave
-// owns 32 of them.  K and V tiles of 64 keys are staged through LDS (two
-// stages; V is stored transposed, d-major).  Per tile a wave computes
-// S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K as the A operand), so that every
-// lane holds 16 scores of ONE query row: the running max and sum of that row
-// live in the lane, P^T feeds the next MFMA straight from the lane's registers,
-// and O^T = V^T P^T leaves the output of the same query row in the same lane.
-// The key order inside each 32-key block is permuted (bits 2 and 3 of the key
-// index swapped) so that the 8 keys a lane contributes to a PV MFMA are
-// contiguous in the transposed V tile (one 16-byte LDS read).  Softmax runs in
-// fp32 with exp2 and the log2(e) folded into the scale; P is rounded to bf16
-// for the PV product.
+// bf16, head_dim 128: flash-style kernel for gfx950.  One 256-thread
+// workgroup (4 waves, one per SIMD) owns 256 query rows of one (request,
+// head); each wave owns 64 of them, so every K/V byte read from LDS feeds 64
+// queries.  K and V tiles of 32 keys stream from global memory straight into
+// an LDS ring of 8 tiles (buffer loads with the lds modifier: no registers,
+// no LDS store instructions), issued 7 tiles ahead of use.  Both are stored
+// row-major with their 16-byte chunks XOR-swizzled per row.
+//
+// Per tile a wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K as
+// the A operand, Q fragments held in registers), so every lane holds the
+// scores of its query rows: P^T feeds the PV MFMA straight from the lane's
+// registers, and O^T = V^T P^T leaves the output of the same rows in the same
+// lane.  The V^T operand is read from the row-major V tile with the
+// transposing LDS read (ds_read_b64_tr_b16); its source rows are chosen so
+// that the 8 keys a lane contributes match the order of the lane's scores
+// (bits 2 and 3 of the key index swapped).
+//
+// The loop is software-pipelined in half steps of one query block (32 rows):
+// while the matrix core computes S of the next tile for one block and the PV
+// product of the current tile, the vector ALU runs the softmax of the other
+// block's finished scores.  Softmax is fp32 with exp2 and log2(e) folded into
+// the scale, against a per-row reference fixed for the whole pass (the first
+// tile's row max): no rescale of O inside the loop.  The pass also tracks the
+// true row max; if any row of the workgroup exceeded its reference by more
+// than 2^64 (where the probabilities could overflow), the work item is
+// recomputed with the exact max as reference, so the result is always the
+// exact softmax up to rounding.
 //
 // fp32: one thread per (query row, head) with an exact online softmax.
 #include <type_traits>
@@ -25,23 +39,18 @@ namespace dit {
 
 namespace {
 
-constexpr int D = 128;           // head_dim of the bf16 kernel
-constexpr int BQ = 256;          // query rows per workgroup
-constexpr int BKV = 64;          // keys per LDS tile
-constexpr int kWaves = 8;
+constexpr int D = 128;                 // head_dim of the bf16 kernel
+constexpr int BQ = 256;                // query rows per workgroup
+constexpr int BKV = 32;                // keys per tile
+constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-// K rows (one key, 256 B) are padded to a 272-byte pitch, so that fragment
-// reads of 8 or 16 consecutive rows hit distinct banks and every K fragment
-// address is a per-lane base plus an immediate.  V^T rows (one d, 64 keys =
-// 128 B) are unpadded; their 16-byte chunks are XOR-swizzled with
-// vt_swizzle(d), conflict-free both for the transposing writes and for the
-// fragment reads.
-constexpr int kKPitch = D * 2 + 16;
-constexpr int kVPitch = BKV * 2;
-constexpr int kKBytes = BKV * kKPitch;   // 17 KiB
-constexpr int kVSlots = 3;               // V^T tiles live one step longer than K tiles
-constexpr int kVBytes = D * kVPitch;     // 18 KiB
+constexpr int kRing = 8;               // LDS ring of K/V tiles
+constexpr int kTileBytes = BKV * D * 2;          // one K or V tile (8 KiB)
+constexpr int kSlotBytes = 2 * kTileBytes;       // K tile + V tile
+constexpr int kPieces = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave and operand (2)
+constexpr int kLoadsPerTile = 2 * kPieces;       // this wave's loads of one tile
 constexpr int kXcds = 8;
+constexpr float kHeadroom = 64.0f;   // log2 units; probabilities stay below 2^64
 
 struct AttnWork {
   int n_req;                        // requests, in scheduling order (longest first)
@@ -53,26 +62,65 @@ struct AttnWork {
   int prefix[DIT_MAX_REQ + 1];      // work items before request i (all heads)
 };
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+// Raw buffer descriptor over `bytes` bytes from `base`: loads past the end
+// return zeros.
+__device__ __forceinline__ u32x4 make_desc(const void* base, int64_t bytes) {
+  const uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
+  const uint64_t p = (uint64_t)base;
+  return u32x4{(uint32_t)p, (uint32_t)(p >> 32) & 0xFFFFu, n, 0x00020000u};
 }
 
-__device__ __forceinline__ int vt_swizzle(int d) { return (d & 7) ^ ((d >> 3) & 3); }
-
-// swap bits 2 and 3 of a key index inside its 16-key group
-__device__ __forceinline__ int perm23(int x) {
-  return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1);
+// 16 bytes per lane from global memory straight into LDS: lane i writes LDS
+// bytes lds + 16 i .. +15.  Inline assembly, so the compiler does not make
+// every later LDS read wait for it; completion is tracked by hand
+// (wait_vmcnt) and the workgroup barrier publishes the data.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_lds16(const u32x4& desc, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds), "v"(voff), "s"(desc) : "m0");
 }
+#pragma clang diagnostic pop
+template <int N> __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N)); }
+
+// wait until at most `tiles` of this wave's most recently issued tiles are pending
+__device__ __forceinline__ void wait_tiles(int tiles) {
+  if (tiles <= 0) wait_vmcnt<0>();
+  else if (tiles == 1) wait_vmcnt<1 * kLoadsPerTile>();
+  else if (tiles == 2) wait_vmcnt<2 * kLoadsPerTile>();
+  else if (tiles == 3) wait_vmcnt<3 * kLoadsPerTile>();
+  else if (tiles == 4) wait_vmcnt<4 * kLoadsPerTile>();
+  else if (tiles == 5) wait_vmcnt<5 * kLoadsPerTile>();
+  else if (tiles == 6) wait_vmcnt<6 * kLoadsPerTile>();
+  else wait_vmcnt<7 * kLoadsPerTile>();
+}
+
+// S^T MFMAs of the main loop as inline assembly with vector-register
+// operands: the compiler would otherwise place the scores in accumulation
+// registers and copy them to vector registers for the softmax.  It does not
+// see these as MFMAs, so the distance from the last MFMA of a score block to
+// its first vector read is kept by hand: score_guard (at least 19 wait
+// states) takes the block as an in-out operand, so no read of it can be
+// scheduled before the guard.
+__device__ __forceinline__ void mfma_s_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  // d as an in-out operand (its old value unused) keeps the scores in the
+  // same registers from tile to tile, without copies
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "+v"(d) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_s_acc(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void score_guard(f32x16& d) { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4" : "+v"(d)); }
+
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
     float scale_log2, AttnWork work) {
-  // K(j) in K slot j & 1, V(j) in V slot j % 3
-  __shared__ __attribute__((aligned(16))) char smem[2 * kKBytes + kVSlots * kVBytes];
-  char* const kslots = smem;
-  char* const vslots = smem + 2 * kKBytes;
+  // slot t % kRing holds K(t) (first 8 KiB) and V(t)
+  __shared__ __attribute__((aligned(1024))) char smem[kRing * kSlotBytes];
 
   // ---- work item: XCD-contiguous numbering, requests longest first
   const int nb = gridDim.x;
@@ -95,255 +143,312 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   const int fr = lane & 31;
   const int fh = lane >> 5;
 
-  // ---- Q fragments (MFMA B operand of S^T): row fr of this wave, d 16kk + 8fh .. +7
-  const int my_q = q0 + wave * 32 + fr;
-  bf16x8 qf[8];
-  {
-    const int qrow = min(my_q, q_end - 1);
+  // ---- Q fragments (B operand of S^T): query q0 + 64 wave + 32 qb + fr,
+  // d 16 kc + 8 fh .. +7
+  bf16x8 qf[2][8];
+  int my_q[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    my_q[qb] = q0 + 64 * wave + 32 * qb + fr;
+    const int qrow = min(my_q[qb], q_end - 1);
     const bf16* qp = Q + (int64_t)qrow * qs + head * D + 8 * fh;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + 16 * kk);
+    for (int kc = 0; kc < 8; ++kc) qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qp + 16 * kc);
   }
+  // the Q loads complete here, before any tile load is issued (otherwise the
+  // compiler's wait for them would also wait for the tile loads, in the loop)
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 
-  // ---- global -> LDS staging (all 512 threads share every tile)
-  // buffer resources are rebased at every tile so offsets stay small; loads
-  // past the request's last key return zeros
+  // ---- global -> LDS.  A tile (K or V) is 8 pieces of 1 KiB = 4 key rows of
+  // 256 B; wave w loads pieces 2 w, 2 w + 1 of both.  Lane i of piece p
+  // fills LDS chunk i of the piece: row 4 p + i / 16, physical chunk i % 16,
+  // which holds logical chunk (i % 16) ^ swizzle(row):
+  //   K: swizzle(row) = row % 16   (fragment reads of 16 rows at one chunk)
+  //   V: swizzle(row) = 4 (row % 4) (transposing reads of 4 rows x 64 B)
   const bf16* k_head = K + (int64_t)k0 * ks + head * D;
   const bf16* v_head = V + (int64_t)k0 * vs + head * D;
-  // K: 2 chunks of 16 B per thread: key (tid >> 4) + 32 i, chunk tid & 15;
-  // key k is stored in row slot perm23(k) so that MFMA row fr reads slot fr
-  const int kl_key = tid >> 4;
-  const int kl_c = tid & 15;
-  const int kl_voff = kl_key * (int)ks * 2 + kl_c * 16;
-  const int kl_st = perm23(kl_key) * kKPitch + kl_c * 16;   // + 32 kKPitch for i = 1
-  // V: keys 4 kg .. 4 kg + 3, d 4 dc .. 4 dc + 3 (8-byte loads; a wave reads
-  // two whole 256-byte key rows per load), written transposed as V^T
-  const int vl_lo = tid & 1;
-  const int vl_dc = (tid >> 1) & 31;
-  const int vl_kg = 2 * (tid >> 6) + vl_lo;
-  const int vl_voff = (4 * vl_kg) * (int)vs * 2 + vl_dc * 8;
-  int vl_st[4];
+  uint32_t k_voff[kPieces], v_voff[kPieces];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int d = 4 * vl_dc + e;
-    vl_st[e] = d * kVPitch + (((vl_kg >> 1) ^ vt_swizzle(d)) << 4) + (vl_kg & 1) * 8;
+  for (int u = 0; u < kPieces; ++u) {
+    const int row = 4 * (kPieces * wave + u) + (lane >> 4);
+    const int pc = lane & 15;
+    k_voff[u] = (uint32_t)(row * (int)ks * 2 + ((pc ^ (row & 15)) << 4));
+    v_voff[u] = (uint32_t)(row * (int)vs * 2 + ((pc ^ (4 * (row & 3))) << 4));
   }
-
-  // two register staging sets: the loads of tile t go to set t & 1, two
-  // steps before the tile is read from LDS
-  u32x4 kreg[2][2];
-  u32x2 vreg[2][4];
-  auto gload = [&](int kt, auto set) {
-    constexpr int S = decltype(set)::value;
-    const int kb0 = kt * BKV;
-    const __amdgpu_buffer_rsrc_t krs = make_rsrc(k_head + (int64_t)kb0 * ks, (int64_t)(n_k - kb0) * ks * 2);
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_char*)smem;
+  auto issue = [&](int t) {
+    const int kb = t * BKV;
+    const u32x4 kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
+    const u32x4 vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
+    const uint32_t st = lds_base + (uint32_t)((t % kRing) * kSlotBytes) + kPieces * wave * 1024;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      kreg[S][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, kl_voff, 32 * i * (int)ks * 2, 0);
-    // keys past the request end lie past the end of the buffer range and load
-    // as zeros, so P = 0 times V stays exact (no select on the loaded value,
-    // which would wait for the load right here)
-    const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v_head + (int64_t)kb0 * vs, (int64_t)(n_k - kb0) * vs * 2);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      vreg[S][i] = __builtin_amdgcn_raw_buffer_load_b64(vrs, vl_voff, i * (int)vs * 2, 0);
-  };
-  auto sstore = [&](int kt, auto set) {
-    constexpr int S = decltype(set)::value;
-    char* kb = kslots + (kt & 1) * kKBytes;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(kb + kl_st + 32 * i * kKPitch) = kreg[S][i];
-    char* vb = vslots + (kt % kVSlots) * kVBytes;
-    // transpose 4 keys x 4 d: element (key i, d e) -> V^T[d e][key i]
-    const uint16_t* vv = reinterpret_cast<const uint16_t*>(vreg[S]);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      u32x2 t;
-      t[0] = (uint32_t)vv[0 * 4 + e] | ((uint32_t)vv[1 * 4 + e] << 16);
-      t[1] = (uint32_t)vv[2 * 4 + e] | ((uint32_t)vv[3 * 4 + e] << 16);
-      *reinterpret_cast<u32x2*>(vb + vl_st[e]) = t;
+    for (int u = 0; u < kPieces; ++u) {
+      load_lds16(kd, k_voff[u], st + u * 1024);
+      load_lds16(vd, v_voff[u], st + kTileBytes + u * 1024);
     }
   };
 
-  // ---- fragment read offsets inside a slot
-  // K (A operand of S^T): slot 32 blk + fr (= key 32 blk + perm23(fr)), d 16 kk + 8 fh
-  const int koff = fr * kKPitch + fh * 16;             // + blk 32 kKPitch + kk 32
-  // V^T (A operand of O^T): row d = 32 dblk + fr, 16-byte chunk 2 (2 blk + hs) + fh
-  // (vt_swizzle(32 dblk + fr) == vt_swizzle(fr))
-  int voff[4];                                         // [2 blk + hs], + dblk 32 kVPitch
-#pragma unroll
-  for (int c4 = 0; c4 < 4; ++c4) voff[c4] = fr * kVPitch + (((2 * c4 + fh) ^ vt_swizzle(fr)) << 4);
+  // ---- fragment addresses inside a slot
+  // K (A operand of S^T): row fr, logical chunk 2 kc + fh:
+  //   fr * 256 + (((2 kc + fh) ^ (fr % 16)) << 4) = k_lane ^ (kc << 5)
+  const int k_lane = fr * 256 + ((fh ^ (fr & 15)) << 4);
+  // V^T (A operand of O^T) by transposing reads.  Lanes 16 g .. 16 g + 15
+  // (h = g / 2, dh = g % 2) fetch d 32 db + 16 dh .. +15 of 4 key rows; source
+  // lane s reads row 16 kc + 4 h + 8 half + s / 4, d 32 db + 16 dh + 4 (s % 4)
+  // .. +3 (8 bytes), and lane s receives d 32 db + 16 dh + s of those 4 keys.
+  // Logical chunk 4 db + 2 dh + (s / 2) % 2 lies at physical chunk
+  // (that) ^ 4 (s / 4), i.e. v_lane ^ (db << 6) plus the row offset.
+  int v_lane;
+  {
+    const int s16 = lane & 15, g = lane >> 4;
+    const int h = g >> 1, dh = g & 1, m = s16 >> 2;
+    v_lane = kTileBytes + (4 * h + m) * 256 + 64 * m + 16 * (2 * dh + ((s16 >> 1) & 1)) + 8 * (s16 & 1);
+  }
 
   const int n_tiles = (n_k + BKV - 1) / BKV;
-  const int n_full = n_k / BKV;
+  const bool ragged = n_k % BKV != 0;
+  // Scores of one query block of a tile: S[4 i + j] = S[key 8 i + 4 fh + j][query 32 qb + fr]
+  f32x16 sq[2];         // sq[qb]: scores of the query block being computed or softmaxed
+  bf16x8 pq[2][2];      // pq[qb][kc]: P^T operand, probabilities of scores 8 kc .. 8 kc + 7
+  f32x16 oacc[4][2];    // oacc[db][qb][4 i + j] = O[query 32 qb + fr][d 32 db + 8 i + 4 fh + j]
+  // Softmax reference of the lane's rows (log2 units): P = 2^(score - m_ref).
+  // It is fixed for the whole pass (no O rescale inside the loop); x_max
+  // tracks max(score - m_ref).  While that stays <= kHeadroom the
+  // probabilities stay below 2^kHeadroom and the pass is exact; otherwise the
+  // work item is computed again with m_ref = the exact row max.
+  float m_ref[2], x_max[2];
+  float l_run[2];       // this lane's share of the row sums (of the bf16 probabilities)
 
-  f32x16 oacc[4];
+  // keys past the request end (ragged last tile) score -inf
+  auto mask = [&](int t, f32x16& a) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) oacc[i] = f32x16{};
-  f32x16 s[2];          // scores of the current tile: s[blk][4i + j] = S[q = fr][key 32 blk + perm23(8 i + 4 fh + j)]
-  bf16x8 pf[2][2];      // probabilities of the current tile, PV operand
-  float m_tile = 0.f;   // max of the current tile's scores of the lane's row (times scale_log2)
-  // Running max of (score * scale_log2) of the lane's query row.  It is only
-  // raised when a tile's max exceeds it by more than kLazy (log2 units), so
-  // that the O rescale is skipped for most tiles; probabilities are then
-  // bounded by 2^kLazy, harmless in fp32 and bf16.
-  constexpr float kLazy = 8.0f;
-  float m_run = -INFINITY;
-  float l_run = 0.f;    // this lane's share of the running sum
-
-  // S(j) = K(j) Q^T, as four independent MFMA chains (even and odd d-steps of
-  // each 32-key block) summed at the end, so that no MFMA waits on the result
-  // of the one issued just before it
-  auto mma_s = [&](int j) {
-    const char* kb = kslots + (j & 1) * kKBytes + koff;
-    f32x16 s2[2][2];
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + blk * 32 * kKPitch + kk * 32);
-        s2[blk][kk & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], kk < 2 ? f32x16{} : s2[blk][kk & 1], 0, 0, 0);
-      }
+    for (int v = 0; v < 16; ++v) {
+      const int key = t * BKV + 8 * (v >> 2) + 4 * fh + (v & 3);
+      if (key >= n_k) a[v] = -INFINITY;
     }
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) s[blk] = s2[blk][0] + s2[blk][1];
-    // keep four fragment reads in flight ahead of the MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
-#pragma unroll
-    for (int i = 0; i < 12; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
   };
-  // O^T += V^T(j) P^T(j)
-  auto mma_pv = [&](int j) {
-    const char* vb = vslots + (j % kVSlots) * kVBytes;
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int hs = 0; hs < 2; ++hs)
-#pragma unroll
-        for (int dblk = 0; dblk < 4; ++dblk) {
-          bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + voff[2 * blk + hs] + dblk * 32 * kVPitch);
-          oacc[dblk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[blk][hs], oacc[dblk], 0, 0, 0);
-        }
-    // keep four fragment reads in flight ahead of the MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
-#pragma unroll
-    for (int i = 0; i < 12; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
+  // softmax pair j (0 .. 7) of query block qb: scores 2 j, 2 j + 1 -> pq[qb][j / 4]
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  auto soft_pair = [&](int qb, int j) {
+    const int kc = j >> 2, e = 2 * (j & 3);
+    const float x0 = fmaf(sq[qb][2 * j], scale_log2, -m_ref[qb]);
+    const float x1 = fmaf(sq[qb][2 * j + 1], scale_log2, -m_ref[qb]);
+    x_max[qb] = fmaxf(fmaxf(x_max[qb], x0), x1);
+    const bf16x2 pr = __builtin_convertvector(
+        (f32x2){__builtin_amdgcn_exp2f(x0), __builtin_amdgcn_exp2f(x1)}, bf16x2);
+    pq[qb][kc][e] = pr[0];
+    pq[qb][kc][e + 1] = pr[1];
+    // the row sum adds the rounded probabilities, the ones the PV product uses
+    const bf16x2 one2 = {(bf16)1.0f, (bf16)1.0f};
+    l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, l_run[qb], false);
   };
-  // mask of the ragged last tile (masked == true), then the row max of S(j)
-  auto row_max = [&](int j, auto masked) {
-    if (decltype(masked)::value) {
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = j * BKV + 32 * blk + perm23(8 * (v >> 2) + 4 * fh + (v & 3));
-          if (key >= n_k) s[blk][v] = -INFINITY;
-        }
-    }
-    // the lane's 32 scores, then the other half-wave's 32 (same row)
-    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
-#pragma unroll
-    for (int v = 3; v < 15; v += 2) mx = fmaxf(fmaxf(mx, s[0][v]), s[0][v + 1]);
-    mx = fmaxf(mx, s[0][15]);
-#pragma unroll
-    for (int v = 0; v < 16; v += 2) mx = fmaxf(fmaxf(mx, s[1][v]), s[1][v + 1]);
-    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-    m_tile = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+  // the softmax results of a half step are computed before its end, not sunk
+  // into the next half step (where the compiler would otherwise move them)
+  auto fence_soft = [&](int qb) {
+    asm volatile("" :: "v"(pq[qb][0]), "v"(pq[qb][1]), "v"(l_run[qb]), "v"(x_max[qb]));
   };
-  // online softmax of S into P
-  auto softmax = [&]() {
-    if (__builtin_amdgcn_ballot_w64(m_tile > m_run + kLazy) != 0) {
-      const float m_new = fmaxf(m_run, m_tile);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
-    }
-    float psum = 0.f;
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale_log2, -m_run));
-        psum += p;
-        pf[blk][v >> 3][v & 7] = (bf16)p;
-      }
-    l_run += psum;
+  auto v_frag = [&](int so, int m) {   // V^T fragment m = 4 kc + db of a slot
+    const int ad = so + (v_lane ^ ((m & 3) << 6)) + (m >> 2) * 16 * 256;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad + 8 * 256));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  // ---- main loop.  Step j computes tile j from LDS, issues the loads of
-  // tile j+2 (register set j & 1) at its start and stores tile j+1 (loaded
-  // one step earlier, set (j+1) & 1) to LDS before its barrier, so every load
-  // has two steps to arrive.  Full tiles inside the loop (unrolled by two for
-  // the register sets), the ragged last tile (with its key mask) after it.
-  // Waves 0-3 run S(j), softmax(j), PV(j) between two barriers.  Waves 4-7
-  // run the same sequence but take the barrier before PV(j), which they
-  // compute at the start of the next step: the two waves sharing a SIMD are
-  // then half a step apart, one on the matrix core while the other runs its
-  // softmax.  V(j) is read until the step after j, hence three V slots.
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  gload(0, S0{});
-  sstore(0, S0{});
-  if (n_tiles > 1) gload(1, S1{});
-  // every load issued so far (Q fragments included) has completed: without
-  // this the waits for the Q loads land inside the loop, where they would
-  // also wait for each step's K and V prefetch
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-  __syncthreads();
-  const bool lead = wave < kWaves / 2;
-  auto step_full = [&](int j, auto set) {
-    constexpr int S = decltype(set)::value;
-    if (j + 2 < n_tiles) gload(j + 2, std::integral_constant<int, S>{});
-    if (!lead && j > 0) mma_pv(j - 1);
-    mma_s(j);
-    row_max(j, std::false_type{});
-    softmax();
-    if (lead) mma_pv(j);
-    if (j + 1 < n_tiles) sstore(j + 1, std::integral_constant<int, 1 - S>{});
+  // steady state (step t loaded tile t + kRing - 1 < n_tiles): tiles up to
+  // t + 2 are needed next, so kRing - 3 tiles may stay in flight
+  auto end_of_step_steady = [&]() {
+    wait_vmcnt<(kRing - 3) * kLoadsPerTile>();
     __syncthreads();
   };
-  int j = 0;
-  for (; j + 2 <= n_full; j += 2) {
-    step_full(j, S0{});
-    step_full(j + 1, S1{});
-  }
-  if (j < n_full) {
-    step_full(j, S0{});
-    ++j;
-  }
-  if (!lead && n_full > 0) mma_pv(n_full - 1);
-  if (n_full < n_tiles) {
-    mma_s(n_full);
-    row_max(n_full, std::true_type{});
-    softmax();
-    mma_pv(n_full);
+  auto end_of_step = [&](int t) {
+    // tiles up to t + 2 in LDS for the next step (V(t + 1), K(t + 2)); tiles
+    // up to t + kRing - 1 have been issued
+    wait_tiles(min(t + kRing - 1, n_tiles - 1) - min(t + 2, n_tiles - 1));
+    __syncthreads();
+  };
+
+  // Step t, two halves of 8 slots (half h works on query block h):
+  //   slot 8 h + i: one MFMA of S(t + 1) for block h (d-chunk i)
+  //                 one MFMA of O += V(t) P(t) for block h (V^T fragment i)
+  //                 softmax pair i of the other block's scores:
+  //                   half 0: S(t) block 1 -> P(t) block 1 (used by half 1)
+  //                   half 1: S(t + 1) block 0 (just computed) -> P(t + 1) block 0
+  // K and V^T fragments are read in half 0, 2 and 1 slots ahead, and kept for
+  // half 1.  Only one score block per query block is live at any time.
+  //   WITH_S: compute S(t + 1)  (false for the last tile)
+  //   MASKED: tile t + 1 is the ragged last tile
+  auto step = [&](int t, auto with_s, auto masked, int load_tile) {
+    constexpr bool WS = decltype(with_s)::value;
+    constexpr bool MK = decltype(masked)::value;
+    u32x4 kd{}, vd{};
+    uint32_t st = 0;
+    if (load_tile >= 0) {
+      const int kb = load_tile * BKV;
+      kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
+      vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
+      st = lds_base + (uint32_t)((load_tile % kRing) * kSlotBytes) + kPieces * wave * 1024;
+    }
+    const int so_k = ((t + 1) % kRing) * kSlotBytes + k_lane;
+    const int so_v = (t % kRing) * kSlotBytes;
+    bf16x8 kf[8], vf[8];
+    if (WS) {
+      kf[0] = *reinterpret_cast<const bf16x8*>(smem + so_k);
+      kf[1] = *reinterpret_cast<const bf16x8*>(smem + (so_k ^ (1 << 5)));
+    }
+    vf[0] = v_frag(so_v, 0);
+    score_guard(sq[1]);   // S(t) block 1 was finished at the end of the previous step
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int sl = 0; sl < 16; ++sl) {
+      const int h = sl >> 3, i = sl & 7;
+      if (h == 0) {
+        if (WS && i + 2 < 8) kf[i + 2] = *reinterpret_cast<const bf16x8*>(smem + (so_k ^ ((i + 2) << 5)));
+        if (i + 1 < 8) vf[i + 1] = v_frag(so_v, i + 1);
+      }
+      if (WS) {
+        if (i == 0) mfma_s_first(sq[h], kf[i], qf[h][i]);
+        else mfma_s_acc(sq[h], kf[i], qf[h][i]);
+      }
+      oacc[i & 3][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pq[h][i >> 2], oacc[i & 3][h], 0, 0, 0);
+      if (sl == 8) {
+        // S(t + 1) block 0 is complete: mask it if it is the ragged last tile,
+        // then wait out the matrix-core latency before reading it
+        if (MK && ragged) mask(t + 1, sq[0]);
+        score_guard(sq[0]);
+      }
+      if (h == 0) soft_pair(1, i);
+      else if (WS) soft_pair(0, i);
+      if (load_tile >= 0 && (sl & 3) == 1) {
+        const int u = sl >> 3, v = (sl >> 2) & 1;   // K piece 0, V piece 0, K piece 1, V piece 1
+        if (v == 0) load_lds16(kd, k_voff[u], st + u * 1024);
+        else load_lds16(vd, v_voff[u], st + kTileBytes + u * 1024);
+      }
+      if (sl == 7) fence_soft(1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (WS) {
+      fence_soft(0);
+      if (MK && ragged) {
+        score_guard(sq[1]);
+        mask(t + 1, sq[1]);
+      }
+    }
+  };
+  using kOn = std::true_type;
+  using kOff = std::false_type;
+
+  __shared__ int redo_flag;
+  for (int pass = 0;; ++pass) {
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = f32x16{};
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      l_run[qb] = 0.f;
+      x_max[qb] = -INFINITY;
+    }
+    const int n_pre = min(kRing, n_tiles);
+    for (int t = 0; t < n_pre; ++t) issue(t);
+    // tiles 0 and 1 in LDS (K(0), K(1), V(0))
+    wait_tiles(n_pre - 1 - min(1, n_tiles - 1));
+    if (pass == 0 && tid == 0) redo_flag = 0;
+    __syncthreads();
+
+    if (n_tiles > 0) {
+      // S(0), both query blocks
+      {
+        const int so = k_lane;
+#pragma unroll
+        for (int kc = 0; kc < 8; ++kc) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(smem + (so ^ (kc << 5)));
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            if (kc == 0) mfma_s_first(sq[qb], kf, qf[qb][kc]);
+            else mfma_s_acc(sq[qb], kf, qf[qb][kc]);
+          }
+        }
+        score_guard(sq[0]);
+        score_guard(sq[1]);
+      }
+      if (n_tiles == 1 && ragged) {
+        mask(0, sq[0]);
+        mask(0, sq[1]);
+      }
+      if (pass == 0) {
+        // reference: the row max of the first tile
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          float mx = sq[qb][0];
+#pragma unroll
+          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sq[qb][v]);
+          auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+          m_ref[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) soft_pair(0, j);   // P(0) block 0
+    }
+    // Step t loads tile t + kRing - 1 into the slot of tile t - 1 (free since
+    // the barrier that ended step t - 1); step 0 has nothing to load, the
+    // prologue filled every slot.
+    int t = 0;
+    if (t + 2 < n_tiles) {
+      step(0, kOn{}, kOff{}, -1);
+      end_of_step(0);
+      t = 1;
+    }
+    // no compiler-tracked load may still be pending when the steady loop
+    // starts: its tracking would otherwise put a vmcnt wait (which also waits
+    // for the tile loads in flight) at the top of every iteration
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
+    for (; t + kRing < n_tiles; ++t) {      // loads every step, constant wait count
+      step(t, kOn{}, kOff{}, t + kRing - 1);
+      end_of_step_steady();
+    }
+    for (; t + 2 < n_tiles; ++t) {
+      step(t, kOn{}, kOff{}, t + kRing - 1 < n_tiles ? t + kRing - 1 : -1);
+      end_of_step(t);
+    }
+    if (t + 1 < n_tiles) {   // S of the last tile (t + 1), which may be ragged
+      step(t, kOn{}, kOn{}, -1);
+      end_of_step(t);
+      ++t;
+    }
+    if (t < n_tiles) step(t, kOff{}, kOff{}, -1);   // the last tile: PV only
+    if (pass == 1) break;
+    // did any row of the workgroup exceed its reference by more than the headroom?
+    float xm[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x_max[qb]), __float_as_uint(x_max[qb]), false, false);
+      xm[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const bool over = xm[0] > kHeadroom || xm[1] > kHeadroom;
+    if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) redo_flag = 1;
+    __syncthreads();
+    if (redo_flag == 0) break;
+    m_ref[0] += xm[0];
+    m_ref[1] += xm[1];
   }
 
-  // ---- normalise and store: oacc[dblk][4i + j] = O[q = fr][d = 32 dblk + 8 i + 4 fh + j]
-  // (the S^T rows of a lane are keys perm23(8 i + 4 fh + j); for the PV MFMA of
-  // half hs the lane's 8 values are keys 16 hs + 8 fh + 0..7 of the block)
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
-  if (my_q < q_end) {
-    bf16* op = O + (int64_t)my_q * os + head * D + 4 * fh;
+  // ---- normalise and store
 #pragma unroll
-    for (int dblk = 0; dblk < 4; ++dblk)
+  for (int qb = 0; qb < 2; ++qb) {
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run[qb]), __float_as_uint(l_run[qb]), false, false);
+    const float l_tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
+    if (my_q[qb] < q_end) {
+      bf16* op = O + (int64_t)my_q[qb] * os + head * D + 4 * fh;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16x4 ov;
+      for (int db = 0; db < 4; ++db)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) ov[j] = (bf16)(oacc[dblk][4 * i + j] * inv);
-        *reinterpret_cast<bf16x4*>(op + 32 * dblk + 8 * i) = ov;
-      }
+        for (int i = 0; i < 4; ++i) {
+          bf16x4 ov;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) ov[j] = (bf16)(oacc[db][qb][4 * i + j] * inv);
+          *reinterpret_cast<bf16x4*>(op + 32 * db + 8 * i) = ov;
+        }
+    }
   }
 }
 

@@ -185,6 +185,30 @@ def test_attention_varlen(dtype, H, d, lq, lk):
     check(host(out), ref, dtype, "attention")
 
 
+@pytest.mark.parametrize("jump_key", [100, 1999])
+def test_attention_late_score_jump(jump_key):
+    """A key far past the first tile whose score exceeds every earlier one by
+    far more than the kernel's softmax headroom (2^64): the workgroup must
+    detect it and recompute with the exact row max."""
+    B = require_gpu()
+    log(f"case attention late score jump key={jump_key}")
+    H, d, n = 2, 128, 2048
+    W = H * d
+    qkv = synth.draw((n, 3 * W), (33, jump_key), "bf16").copy()
+    half = np.float32(0.5).view(np.uint32) >> 16          # bf16 bits of 0.5
+    big = np.float32(20.0).view(np.uint32) >> 16
+    qkv[:, :W] = half                                      # every query = 0.5 * ones
+    qkv[jump_key, W:2 * W] = big                           # one key = 20 * ones: score ~ +82 (log2 units)
+    t = dev(qkv)
+    out = empty((n, W), "bf16")
+    cu = [0, n]
+    B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], out, cu, cu, H, d)
+    torch.cuda.synchronize()
+    x = O.decode(qkv)
+    ref = O.attention_varlen(x[:, :W], x[:, W:2 * W], x[:, 2 * W:], cu, cu, H, d)
+    check(host(out), ref, "bf16", "attention late jump")
+
+
 def test_attention_varlen_no_leakage():
     """A packed batch equals each request run alone (bitwise: same tiles)."""
     B = require_gpu()
