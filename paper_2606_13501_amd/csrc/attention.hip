@@ -5,9 +5,10 @@
 // workgroup (4 waves, one per SIMD) owns 256 query rows of one (request,
 // head); each wave owns 64 of them, so every K/V byte read from LDS feeds 64
 // queries.  K and V tiles of 32 keys stream from global memory straight into
-// an LDS ring of 8 tiles (buffer loads with the lds modifier: no registers,
-// no LDS store instructions), issued 7 tiles ahead of use.  Both are stored
-// row-major with their 16-byte chunks XOR-swizzled per row.
+// an LDS ring of 4 tiles (buffer loads with the lds modifier: no registers,
+// no LDS store instructions), issued 3 tiles ahead of use; a deeper ring lets
+// the workgroups streaming one head drift further apart and costs L2 hits.
+// Both are stored row-major with their 16-byte chunks XOR-swizzled per row.
 //
 // Per tile a wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K as
 // the A operand, Q fragments held in registers), so every lane holds the
@@ -44,7 +45,7 @@ constexpr int BQ = 256;                // query rows per workgroup
 constexpr int BKV = 32;                // keys per tile
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-constexpr int kRing = 8;               // LDS ring of K/V tiles
+constexpr int kRing = 4;               // LDS ring of K/V tiles
 constexpr int kTileBytes = BKV * D * 2;          // one K or V tile (8 KiB)
 constexpr int kSlotBytes = 2 * kTileBytes;       // K tile + V tile
 constexpr int kPieces = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave and operand (2)
