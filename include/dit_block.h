@@ -201,7 +201,8 @@ dit_status dit_qk_norm_rope(void *q, void *k, int64_t row_stride, int64_t n_rows
 
 /* Standalone gated residual: out[i] = x[i] + gate[r] * (z[i] + bias) for row i
  * of request r; x, z, out [n_rows, hidden]; bias [hidden] (dtype) or NULL;
- * gate device fp32 at gate + r*gate_stride. */
+ * gate device fp32 at gate + r*gate_stride.  hidden <= 8192 (bf16) or 4096
+ * (fp32), else DIT_ERR_UNSUPPORTED.  out may alias x or z. */
 dit_status dit_gated_residual(const void *x, const void *z, const void *bias, const float *gate,
                               int64_t gate_stride, const int32_t *cu_seqlens, int n_req,
                               int hidden, void *out, dit_dtype dtype, hipStream_t stream);

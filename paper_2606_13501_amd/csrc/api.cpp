@@ -580,6 +580,7 @@ dit_status dit_gated_residual(const void* x, const void* z, const void* bias, co
   DIT_TRY(check_cu(cu_seqlens, n_req, "cu_seqlens"));
   const int vec = dtype == DIT_BF16 ? 8 : 4;
   if (hidden < vec || hidden % vec) return fail(DIT_ERR_INVALID_ARG, "hidden %d must be a positive multiple of %d", hidden, vec);
+  if (hidden > (dtype == DIT_BF16 ? 8192 : 4096)) return fail(DIT_ERR_UNSUPPORTED, "hidden %d too large", hidden);
   if (gate_stride < 0 || gate_stride % 4) return fail(DIT_ERR_INVALID_ARG, "gate_stride %lld", (long long)gate_stride);
   GatedResArgs p;
   p.x = x; p.z = z; p.bias = bias; p.gate = gate; p.gate_stride = gate_stride; p.out = out;

@@ -19,13 +19,13 @@ template <typename T> struct Vec16;
 template <> struct Vec16<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
 template <> struct Vec16<float> { typedef f32x4 type; static constexpr int n = 4; };
 
-constexpr int kLnMaxVec = 16;   // 16-byte vectors per lane: D <= 8192 (bf16), 4096 (fp32)
-
 // ------------------------------------------------------------ LayerNorm
 // out = (x - mean) / sqrt(var + eps) * mul + add, one wave per row.
 //   modulate: mul = 1 + scale[req], add = shift[req] (fp32 vectors)
 //   affine:   mul = gamma, add = beta (dtype vectors)
-template <typename T, bool AFFINE>
+// NVL = 16-byte vectors per lane, a compile-time count so the row is held in
+// exactly as many registers as it needs (occupancy hides the HBM latency).
+template <typename T, bool AFFINE, int NVL>
 __global__ __launch_bounds__(256) void layer_norm_kernel(
     const T* __restrict__ x, T* __restrict__ out, int64_t n_rows, int hidden, float eps,
     const float* __restrict__ shift, const float* __restrict__ scale, int64_t mod_stride,
@@ -37,21 +37,21 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(
   if (row >= n_rows) return;
   const int nv = hidden / VN;
   const T* xr = x + row * hidden;
-  V v[kLnMaxVec];
+  V v[NVL];
   float sum = 0.f;
 #pragma unroll
-  for (int i = 0; i < kLnMaxVec; ++i) {
+  for (int i = 0; i < NVL; ++i) {
     const int c = lane + 64 * i;
-    if (c < nv) {
-      v[i] = *reinterpret_cast<const V*>(xr + c * VN);
-#pragma unroll
-      for (int e = 0; e < VN; ++e) sum += to_f<T>(v[i][e]);
-    }
+    v[i] = c < nv ? *reinterpret_cast<const V*>(xr + c * VN) : V{};
   }
+#pragma unroll
+  for (int i = 0; i < NVL; ++i)
+#pragma unroll
+    for (int e = 0; e < VN; ++e) sum += to_f<T>(v[i][e]);
   const float mean = wave_sum(sum) / hidden;
   float sq = 0.f;
 #pragma unroll
-  for (int i = 0; i < kLnMaxVec; ++i) {
+  for (int i = 0; i < NVL; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
 #pragma unroll
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(
   }
   T* orow = out + row * hidden;
 #pragma unroll
-  for (int i = 0; i < kLnMaxVec; ++i) {
+  for (int i = 0; i < NVL; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
       V o;
@@ -97,23 +97,34 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(
 }
 
 // ---------------------------------------------------- QK RMSNorm + rotary
-// One 256-thread block per row.  The rotary cos/sin of the row's head_dim/2
-// pairs are computed once (in double) into LDS and shared by every head of q
-// and k.  A group of head_dim/VN lanes holds one head; its RMS statistic is a
-// shuffle reduction inside the group.
-template <typename T>
+// One wave per row, four rows per 256-thread block.  A head of head_dim
+// values is LPH = head_dim / VN consecutive lanes (LPH divides 64), so every
+// vector a lane touches sits at the same offset inside its head: the lane
+// needs the same VN/2 rotary pairs and the same gain vector for all of them.
+// Lane j computes the cos/sin of pair j (in double) and the lanes gather
+// theirs by shuffles; a head's RMS statistic is a shuffle reduction over its
+// LPH lanes.  q and k vectors of a pass (NV per lane each) are all loaded
+// before any is computed on.
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(
-    T* q, T* k, int64_t row_stride, int n_heads, int head_dim, const T* __restrict__ g_q,
+    T* q, T* k, int64_t row_stride, int64_t n_rows, int n_heads, int head_dim, const T* __restrict__ g_q,
     const T* __restrict__ g_k, float eps, int rope, int sec0, int sec1, int sec2, float theta,
     RopeTable tab) {
   typedef typename Vec16<T>::type V;
   constexpr int VN = Vec16<T>::n;
-  __shared__ float cs[128][2];
-  const int64_t row = blockIdx.x;
-  const int half = head_dim / 2;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lph = head_dim / VN;
+  const int hc = lane % lph;          // chunk index inside the head
+  const int cpt = n_heads * lph;      // vectors per tensor
+  T* base_ptr[2] = {q + row * row_stride, k ? k + row * row_stride : nullptr};
+  const T* gain[2] = {g_q, g_k};
+  float cr[VN / 2], sr[VN / 2];
   if (rope) {
-    if ((int)threadIdx.x < half) {
-      const int j = threadIdx.x;
+    float cj = 1.f, sj = 0.f;
+    const int j = lane;
+    if (j < head_dim / 2) {
       const int r = find_req(tab.cu, tab.n_req, (int)row);
       const int g = tab.offset[r] + (int)row - tab.cu[r];
       const int pt = g / tab.grid_hw[r];
@@ -127,61 +138,69 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(
       const double ang = (double)p * exp(-2.0 * js / ds * log((double)theta));
       double sn, cn;
       sincos(ang, &sn, &cn);
-      cs[j][0] = (float)cn;
-      cs[j][1] = (float)sn;
+      cj = (float)cn;
+      sj = (float)sn;
     }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < VN / 2; ++u) {
+      cr[u] = __shfl(cj, hc * (VN / 2) + u, 64);
+      sr[u] = __shfl(sj, hc * (VN / 2) + u, 64);
+    }
   }
-  const int lanes_per_head = head_dim / VN;
-  const int chunks_per_tensor = n_heads * lanes_per_head;
-  const int n_tensors = k ? 2 : 1;
-  const int total = n_tensors * chunks_per_tensor;
-  // all threads of a wave run the same number of iterations (shuffles below)
-  for (int base = 0; base < total; base += blockDim.x) {
-    const int c = base + threadIdx.x;
-    const bool active = c < total;
-    const int tensor = active ? c / chunks_per_tensor : 0;
-    const int cc = active ? c - tensor * chunks_per_tensor : 0;
-    T* ptr = (tensor ? k : q) + row * row_stride + (int64_t)cc * VN;
-    const T* gain = tensor ? g_k : g_q;
-    const int dpos = (cc % lanes_per_head) * VN;   // offset inside the head
-    V v{};
-    if (active) v = *reinterpret_cast<const V*>(ptr);
-    float f[VN];
+  const int n_t = k ? 2 : 1;
+  for (int b0 = 0; b0 < cpt; b0 += 64 * NV) {
+    V v[2][NV];
 #pragma unroll
-    for (int e = 0; e < VN; ++e) f[e] = to_f<T>(v[e]);
-    if (gain) {
-      float sq = 0.f;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int e = 0; e < VN; ++e) sq += f[e] * f[e];
-      for (int o = lanes_per_head / 2; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
-      const float rs = rsqrtf(sq / head_dim + eps);
-      V g = active ? *reinterpret_cast<const V*>(gain + dpos) : V{};
-#pragma unroll
-      for (int e = 0; e < VN; ++e) f[e] = f[e] * rs * to_f<T>(g[e]);
-    }
-    if (rope) {
-#pragma unroll
-      for (int e = 0; e < VN; e += 2) {
-        const int j = (dpos + e) >> 1;
-        const float cn = cs[j][0], sn = cs[j][1];
-        const float a = f[e], b = f[e + 1];
-        f[e] = a * cn - b * sn;
-        f[e + 1] = a * sn + b * cn;
+      for (int i = 0; i < NV; ++i) {
+        const int c = b0 + lane + 64 * i;
+        v[t][i] = t < n_t && c < cpt ? *reinterpret_cast<const V*>(base_ptr[t] + (int64_t)c * VN) : V{};
       }
-    }
-    if (active) {
-      V o;
 #pragma unroll
-      for (int e = 0; e < VN; ++e) o[e] = from_f<T>(f[e]);
-      *reinterpret_cast<V*>(ptr) = o;
+    for (int t = 0; t < 2; ++t) {
+      if (t >= n_t) break;
+      V g{};
+      if (gain[t]) g = *reinterpret_cast<const V*>(gain[t] + hc * VN);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        if (b0 + 64 * i >= cpt) break;   // wave-uniform
+        const int c = b0 + lane + 64 * i;
+        float f[VN];
+#pragma unroll
+        for (int e = 0; e < VN; ++e) f[e] = to_f<T>(v[t][i][e]);
+        if (gain[t]) {
+          float sq = 0.f;
+#pragma unroll
+          for (int e = 0; e < VN; ++e) sq += f[e] * f[e];
+          for (int o = lph / 2; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
+          const float rs = rsqrtf(sq / head_dim + eps);
+#pragma unroll
+          for (int e = 0; e < VN; ++e) f[e] = f[e] * rs * to_f<T>(g[e]);
+        }
+        if (rope) {
+#pragma unroll
+          for (int u = 0; u < VN / 2; ++u) {
+            const float a = f[2 * u], bb = f[2 * u + 1];
+            f[2 * u] = a * cr[u] - bb * sr[u];
+            f[2 * u + 1] = a * sr[u] + bb * cr[u];
+          }
+        }
+        if (c < cpt) {
+          V o;
+#pragma unroll
+          for (int e = 0; e < VN; ++e) o[e] = from_f<T>(f[e]);
+          *reinterpret_cast<V*>(base_ptr[t] + (int64_t)c * VN) = o;
+        }
+      }
     }
   }
 }
 
 // ------------------------------------------------------- gated residual
-// out = x + gate[req] * (z + bias), one wave per row.
-template <typename T>
+// out = x + gate[req] * (z + bias), one wave per row; the row's x and z
+// vectors (NVL per lane) are all loaded before any is combined.
+template <typename T, int NVL>
 __global__ __launch_bounds__(256) void gated_residual_kernel(
     const T* x, const T* z, const T* __restrict__ bias, const float* __restrict__ gate,
     int64_t gate_stride, T* out, int64_t n_rows, int hidden, ReqTable req) {
@@ -193,20 +212,29 @@ __global__ __launch_bounds__(256) void gated_residual_kernel(
   const int r = find_req(req.cu, req.n_req, (int)row);
   const float* g = gate + (int64_t)r * gate_stride;
   const int nv = hidden / VN;
-  for (int c = lane; c < nv; c += 64) {
-    V xv = *reinterpret_cast<const V*>(x + row * hidden + c * VN);
-    V zv = *reinterpret_cast<const V*>(z + row * hidden + c * VN);
-    V bv{};
-    if (bias) bv = *reinterpret_cast<const V*>(bias + c * VN);
-    V o;
+  V xv[NVL], zv[NVL];
 #pragma unroll
-    for (int e = 0; e < VN; e += 4) {
-      f32x4 g4 = *reinterpret_cast<const f32x4*>(g + c * VN + e);
+  for (int i = 0; i < NVL; ++i) {
+    const int c = lane + 64 * i;
+    xv[i] = c < nv ? *reinterpret_cast<const V*>(x + row * hidden + c * VN) : V{};
+    zv[i] = c < nv ? *reinterpret_cast<const V*>(z + row * hidden + c * VN) : V{};
+  }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        o[e + u] = from_f<T>(to_f<T>(xv[e + u]) + g4[u] * (to_f<T>(zv[e + u]) + to_f<T>(bv[e + u])));
+  for (int i = 0; i < NVL; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nv) {
+      V bv{};
+      if (bias) bv = *reinterpret_cast<const V*>(bias + c * VN);
+      V o;
+#pragma unroll
+      for (int e = 0; e < VN; e += 4) {
+        f32x4 g4 = *reinterpret_cast<const f32x4*>(g + c * VN + e);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          o[e + u] = from_f<T>(to_f<T>(xv[i][e + u]) + g4[u] * (to_f<T>(zv[i][e + u]) + to_f<T>(bv[e + u])));
+      }
+      *reinterpret_cast<V*>(out + row * hidden + c * VN) = o;
     }
-    *reinterpret_cast<V*>(out + row * hidden + c * VN) = o;
   }
 }
 
@@ -267,18 +295,63 @@ __global__ __launch_bounds__(256) void gemv_kernel(const T* __restrict__ W, cons
   }
 }
 
+template <typename T, int NVL>
+hipError_t gres_nvl(const GatedResArgs& p, hipStream_t s) {
+  gated_residual_kernel<T, NVL><<<(unsigned)((p.n_rows + 3) / 4), 256, 0, s>>>(
+      (const T*)p.x, (const T*)p.z, (const T*)p.bias, p.gate, p.gate_stride, (T*)p.out, p.n_rows, p.hidden,
+      p.req);
+  return hipGetLastError();
+}
+
+// Rows of up to 1024 16-byte vectors (8192 bf16, 4096 fp32 values).
 template <typename T>
-hipError_t ln_typed(const LnArgs& p, hipStream_t s) {
+hipError_t gres_typed(const GatedResArgs& p, hipStream_t s) {
+  switch ((p.hidden / Vec16<T>::n + 63) / 64) {
+    case 1: return gres_nvl<T, 1>(p, s);
+    case 2: return gres_nvl<T, 2>(p, s);
+    case 3: case 4: return gres_nvl<T, 4>(p, s);
+    case 5: case 6: return gres_nvl<T, 6>(p, s);
+    case 7: case 8: return gres_nvl<T, 8>(p, s);
+    case 9: case 10: return gres_nvl<T, 10>(p, s);
+    case 11: case 12: return gres_nvl<T, 12>(p, s);
+    case 13: case 14: case 15: case 16: return gres_nvl<T, 16>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T, int NVL>
+hipError_t ln_nvl(const LnArgs& p, hipStream_t s) {
   const unsigned grid = (unsigned)((p.n_rows + 3) / 4);
   if (p.affine)
-    layer_norm_kernel<T, true><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
-                                                    nullptr, nullptr, 0, (const T*)p.gamma,
-                                                    (const T*)p.beta, p.req);
+    layer_norm_kernel<T, true, NVL><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
+                                                         nullptr, nullptr, 0, (const T*)p.gamma,
+                                                         (const T*)p.beta, p.req);
   else
-    layer_norm_kernel<T, false><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
-                                                     p.shift, p.scale, p.mod_stride, nullptr, nullptr,
-                                                     p.req);
+    layer_norm_kernel<T, false, NVL><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
+                                                          p.shift, p.scale, p.mod_stride, nullptr, nullptr,
+                                                          p.req);
   return hipGetLastError();
+}
+
+// Rows of up to 1024 16-byte vectors (8192 bf16, 4096 fp32 values).
+template <typename T>
+hipError_t ln_typed(const LnArgs& p, hipStream_t s) {
+  const int nvl = (p.hidden / Vec16<T>::n + 63) / 64;
+  switch (nvl) {
+    case 1: return ln_nvl<T, 1>(p, s);
+    case 2: return ln_nvl<T, 2>(p, s);
+    case 3: return ln_nvl<T, 3>(p, s);
+    case 4: return ln_nvl<T, 4>(p, s);
+    case 5: return ln_nvl<T, 5>(p, s);
+    case 6: return ln_nvl<T, 6>(p, s);
+    case 7: return ln_nvl<T, 7>(p, s);
+    case 8: return ln_nvl<T, 8>(p, s);
+    case 9: case 10: return ln_nvl<T, 10>(p, s);
+    case 11: case 12: return ln_nvl<T, 12>(p, s);
+    case 13: case 14: return ln_nvl<T, 14>(p, s);
+    case 15: case 16: return ln_nvl<T, 16>(p, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <typename T>
@@ -301,34 +374,38 @@ hipError_t launch_layer_norm(const LnArgs& p, hipStream_t s) {
   return p.dtype == DIT_BF16 ? ln_typed<bf16>(p, s) : ln_typed<float>(p, s);
 }
 
+namespace {
+
+template <typename T, int NV>
+void qk_nv(const NormRopeArgs& p, hipStream_t s) {
+  qk_norm_rope_kernel<T, NV><<<(unsigned)((p.n_rows + 3) / 4), 256, 0, s>>>(
+      (T*)p.q, (T*)p.k, p.row_stride, p.n_rows, p.n_heads, p.head_dim, (const T*)p.g_q, (const T*)p.g_k,
+      p.eps, p.rope, p.sections[0], p.sections[1], p.sections[2], p.theta, p.tab);
+}
+
+template <typename T>
+hipError_t qk_typed(const NormRopeArgs& p, hipStream_t s) {
+  const int64_t nv = ((int64_t)p.n_heads * p.head_dim / Vec16<T>::n + 63) / 64;
+  if (nv <= 1) qk_nv<T, 1>(p, s);
+  else if (nv <= 2) qk_nv<T, 2>(p, s);
+  else if (nv <= 3) qk_nv<T, 3>(p, s);
+  else if (nv <= 4) qk_nv<T, 4>(p, s);
+  else if (nv <= 6) qk_nv<T, 6>(p, s);
+  else if (nv <= 8) qk_nv<T, 8>(p, s);
+  else qk_nv<T, 10>(p, s);   // passes of 10 vectors per lane and tensor
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_qk_norm_rope(const NormRopeArgs& p, hipStream_t s) {
   if (p.n_rows == 0) return hipSuccess;
-  const unsigned grid = (unsigned)p.n_rows;
-  if (p.dtype == DIT_BF16)
-    qk_norm_rope_kernel<bf16><<<grid, 256, 0, s>>>((bf16*)p.q, (bf16*)p.k, p.row_stride, p.n_heads,
-                                                   p.head_dim, (const bf16*)p.g_q, (const bf16*)p.g_k,
-                                                   p.eps, p.rope, p.sections[0], p.sections[1],
-                                                   p.sections[2], p.theta, p.tab);
-  else
-    qk_norm_rope_kernel<float><<<grid, 256, 0, s>>>((float*)p.q, (float*)p.k, p.row_stride, p.n_heads,
-                                                    p.head_dim, (const float*)p.g_q, (const float*)p.g_k,
-                                                    p.eps, p.rope, p.sections[0], p.sections[1],
-                                                    p.sections[2], p.theta, p.tab);
-  return hipGetLastError();
+  return p.dtype == DIT_BF16 ? qk_typed<bf16>(p, s) : qk_typed<float>(p, s);
 }
 
 hipError_t launch_gated_residual(const GatedResArgs& p, hipStream_t s) {
   if (p.n_rows == 0) return hipSuccess;
-  const unsigned grid = (unsigned)((p.n_rows + 3) / 4);
-  if (p.dtype == DIT_BF16)
-    gated_residual_kernel<bf16><<<grid, 256, 0, s>>>((const bf16*)p.x, (const bf16*)p.z,
-                                                     (const bf16*)p.bias, p.gate, p.gate_stride,
-                                                     (bf16*)p.out, p.n_rows, p.hidden, p.req);
-  else
-    gated_residual_kernel<float><<<grid, 256, 0, s>>>((const float*)p.x, (const float*)p.z,
-                                                      (const float*)p.bias, p.gate, p.gate_stride,
-                                                      (float*)p.out, p.n_rows, p.hidden, p.req);
-  return hipGetLastError();
+  return p.dtype == DIT_BF16 ? gres_typed<bf16>(p, s) : gres_typed<float>(p, s);
 }
 
 hipError_t launch_conditioning(const CondArgs& p, hipStream_t s) {

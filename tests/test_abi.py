@@ -116,6 +116,8 @@ def test_norm_kernels_reject_bad_arguments():
     assert L.dit_qk_norm_rope(P, P, 256, 4, 2, 128, P, P, 1e-6, psec, 1e4, None, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
     assert L.dit_qk_norm_rope(P, P, 256, 4, 2, 96, P, P, 1e-6, None, 1e4, None, B.DIT_BF16, S) == B.DIT_ERR_UNSUPPORTED
     assert L.dit_gated_residual(P, P, None, P, 2, pcu, 1, 64, P, B.DIT_BF16, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_gated_residual(P, P, None, P, 64, pcu, 1, 8200, P, B.DIT_BF16, S) == B.DIT_ERR_UNSUPPORTED
+    assert L.dit_gated_residual(P, P, None, P, 64, pcu, 1, 4100, P, B.DIT_F32, S) == B.DIT_ERR_UNSUPPORTED
 
 
 def _block_structs(dtype=B.DIT_BF16, hidden=256, heads=2, head_dim=128, sections=(0, 64, 64)):

@@ -26,7 +26,8 @@ def _req_of(cu):
 
 
 @pytest.mark.parametrize("dtype,D,lengths", [
-    ("bf16", 3072, [5, 1000, 331]), ("bf16", 5120, [1, 257]), ("f32", 384, [64]), ("f32", 384, [3, 20, 41])])
+    ("bf16", 3072, [5, 1000, 331]), ("bf16", 5120, [1, 257]), ("f32", 384, [64]), ("f32", 384, [3, 20, 41]),
+    ("bf16", 8192, [3, 70]), ("bf16", 576, [33]), ("bf16", 1536, [2, 9]), ("f32", 4096, [9]), ("f32", 2816, [5])])
 def test_adaln_modulate(dtype, D, lengths):
     B = require_gpu()
     log(f"case adaln_modulate {dtype} D={D} lengths={lengths}")
@@ -43,7 +44,7 @@ def test_adaln_modulate(dtype, D, lengths):
     check(host(out), ref, dtype, "adaln_modulate")
 
 
-@pytest.mark.parametrize("dtype,D,T", [("bf16", 5120, 777), ("f32", 384, 64)])
+@pytest.mark.parametrize("dtype,D,T", [("bf16", 5120, 777), ("f32", 384, 64), ("bf16", 8192, 37), ("bf16", 704, 50)])
 def test_layer_norm_affine(dtype, D, T):
     B = require_gpu()
     log(f"case layer_norm_affine {dtype} D={D} T={T}")
@@ -115,6 +116,9 @@ def test_linear_inplace_residual():
     ("bf16", 4, 128, (44, 42, 42), [700, 500], [(3, 10, 30), (2, 20, 20)], [0, 100]),
     ("bf16", 3, 128, (0, 64, 64), [1, 300], [(1, 4, 4), (1, 20, 16)], [5, 19]),
     ("f32", 6, 64, (0, 32, 32), [64], [(1, 8, 8)], [0]),
+    ("bf16", 40, 128, (44, 42, 42), [90, 31], [(2, 9, 5), (1, 5, 7)], [0, 3]),
+    ("bf16", 70, 128, (44, 42, 42), [20], [(1, 4, 5)], [0]),
+    ("f32", 100, 64, (20, 22, 22), [17], [(1, 1, 17)], [0]),
 ])
 def test_qk_norm_rope(dtype, H, d, sections, lengths, grids, offsets):
     B = require_gpu()
@@ -231,7 +235,7 @@ def test_attention_varlen_no_leakage():
 # ------------------------------------------------------------ gated residual
 
 
-@pytest.mark.parametrize("dtype,D,lengths", [("bf16", 3072, [10, 500, 3]), ("f32", 384, [64])])
+@pytest.mark.parametrize("dtype,D,lengths", [("bf16", 3072, [10, 500, 3]), ("f32", 384, [64]), ("bf16", 8192, [7, 2]), ("f32", 4096, [5]), ("bf16", 5120, [33])])
 def test_gated_residual(dtype, D, lengths):
     B = require_gpu()
     log(f"case gated_residual {dtype} D={D} lengths={lengths}")
