@@ -31,6 +31,7 @@
 // exact softmax up to rounding.
 //
 // fp32: one thread per (query row, head) with an exact online softmax.
+#include <float.h>
 #include <type_traits>
 
 #include "common.hpp"
@@ -177,7 +178,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     v_voff[u] = (uint32_t)(row * (int)vs * 2 + ((pc ^ (4 * (row & 3))) << 4));
   }
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_char*)smem;
-  auto issue = [&](int t) {
+  auto issue = [&](int t) __attribute__((always_inline)) {
     const int kb = t * BKV;
     const u32x4 kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
     const u32x4 vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
@@ -213,15 +214,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   bf16x8 pq[2][2];      // pq[qb][kc]: P^T operand, probabilities of scores 8 kc .. 8 kc + 7
   f32x16 oacc[4][2];    // oacc[db][qb][4 i + j] = O[query 32 qb + fr][d 32 db + 8 i + 4 fh + j]
   // Softmax reference of the lane's rows (log2 units): P = 2^(score - m_ref).
-  // It is fixed for the whole pass (no O rescale inside the loop); x_max
-  // tracks max(score - m_ref).  While that stays <= kHeadroom the
-  // probabilities stay below 2^kHeadroom and the pass is exact; otherwise the
-  // work item is computed again with m_ref = the exact row max.
+  // It is fixed for the whole pass (no O rescale inside the loop).  The first
+  // pass takes the first tile's row max and checks afterwards that every row
+  // sum l stayed <= 2^kHeadroom (then every probability did, and O cannot
+  // have overflowed).  A row over that bound is computed again: with m_ref
+  // raised by log2(l) when l is finite, which caps its probabilities at 1;
+  // that pass also tracks x_max = max(score - m_ref), so a row whose sum had
+  // overflowed gets m_ref = its exact max in a last pass.
   float m_ref[2], x_max[2];
-  float l_run[2];       // this lane's share of the row sums (of the bf16 probabilities)
+  float l_run[2][2];    // this lane's share of the row sums, two partial sums per block
 
   // keys past the request end (ragged last tile) score -inf
-  auto mask = [&](int t, f32x16& a) {
+  auto mask = [&](int t, f32x16& a) __attribute__((always_inline)) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int key = t * BKV + 8 * (v >> 2) + 4 * fh + (v & 3);
@@ -230,25 +234,26 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   };
   // softmax pair j (0 .. 7) of query block qb: scores 2 j, 2 j + 1 -> pq[qb][j / 4]
   typedef float f32x2 __attribute__((ext_vector_type(2)));
-  auto soft_pair = [&](int qb, int j) {
+  auto soft_pair = [&](int qb, int j, auto track) __attribute__((always_inline)) {
     const int kc = j >> 2, e = 2 * (j & 3);
     const float x0 = fmaf(sq[qb][2 * j], scale_log2, -m_ref[qb]);
     const float x1 = fmaf(sq[qb][2 * j + 1], scale_log2, -m_ref[qb]);
-    x_max[qb] = fmaxf(fmaxf(x_max[qb], x0), x1);
-    const bf16x2 pr = __builtin_convertvector(
-        (f32x2){__builtin_amdgcn_exp2f(x0), __builtin_amdgcn_exp2f(x1)}, bf16x2);
+    if (decltype(track)::value) x_max[qb] = fmaxf(fmaxf(x_max[qb], x0), x1);
+    const float p0 = __builtin_amdgcn_exp2f(x0), p1 = __builtin_amdgcn_exp2f(x1);
+    const bf16x2 pr = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
     pq[qb][kc][e] = pr[0];
     pq[qb][kc][e + 1] = pr[1];
-    // the row sum adds the rounded probabilities, the ones the PV product uses
-    const bf16x2 one2 = {(bf16)1.0f, (bf16)1.0f};
-    l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, l_run[qb], false);
+    // fp32 row sums with plain adds into two independent partial sums (a
+    // bf16 dot-product accumulation here stalls against the MFMAs)
+    l_run[qb][0] += p0;
+    l_run[qb][1] += p1;
   };
   // the softmax results of a half step are computed before its end, not sunk
   // into the next half step (where the compiler would otherwise move them)
-  auto fence_soft = [&](int qb) {
-    asm volatile("" :: "v"(pq[qb][0]), "v"(pq[qb][1]), "v"(l_run[qb]), "v"(x_max[qb]));
+  auto fence_soft = [&](int qb) __attribute__((always_inline)) {
+    asm volatile("" :: "v"(pq[qb][0]), "v"(pq[qb][1]), "v"(l_run[qb][0]), "v"(l_run[qb][1]), "v"(x_max[qb]));
   };
-  auto v_frag = [&](int so, int m) {   // V^T fragment m = 4 kc + db of a slot
+  auto v_frag = [&](int so, int m) __attribute__((always_inline)) {   // V^T fragment m = 4 kc + db of a slot
     const int ad = so + (v_lane ^ ((m & 3) << 6)) + (m >> 2) * 16 * 256;
     const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad));
     const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad + 8 * 256));
@@ -256,11 +261,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   };
   // steady state (step t loaded tile t + kRing - 1 < n_tiles): tiles up to
   // t + 2 are needed next, so kRing - 3 tiles may stay in flight
-  auto end_of_step_steady = [&]() {
+  auto end_of_step_steady = [&]() __attribute__((always_inline)) {
     wait_vmcnt<(kRing - 3) * kLoadsPerTile>();
     __syncthreads();
   };
-  auto end_of_step = [&](int t) {
+  auto end_of_step = [&](int t) __attribute__((always_inline)) {
     // tiles up to t + 2 in LDS for the next step (V(t + 1), K(t + 2)); tiles
     // up to t + kRing - 1 have been issued
     wait_tiles(min(t + kRing - 1, n_tiles - 1) - min(t + 2, n_tiles - 1));
@@ -277,7 +282,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // half 1.  Only one score block per query block is live at any time.
   //   WITH_S: compute S(t + 1)  (false for the last tile)
   //   MASKED: tile t + 1 is the ragged last tile
-  auto step = [&](int t, auto with_s, auto masked, int load_tile) {
+  auto step = [&](int t, auto with_s, auto masked, int load_tile, auto track) __attribute__((always_inline)) {
     constexpr bool WS = decltype(with_s)::value;
     constexpr bool MK = decltype(masked)::value;
     u32x4 kd{}, vd{};
@@ -316,8 +321,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
         if (MK && ragged) mask(t + 1, sq[0]);
         score_guard(sq[0]);
       }
-      if (h == 0) soft_pair(1, i);
-      else if (WS) soft_pair(0, i);
+      if (h == 0) soft_pair(1, i, track);
+      else if (WS) soft_pair(0, i, track);
       if (load_tile >= 0 && (sl & 3) == 1) {
         const int u = sl >> 3, v = (sl >> 2) & 1;   // K piece 0, V piece 0, K piece 1, V piece 1
         if (v == 0) load_lds16(kd, k_voff[u], st + u * 1024);
@@ -337,22 +342,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   using kOn = std::true_type;
   using kOff = std::false_type;
 
-  __shared__ int redo_flag;
-  for (int pass = 0;; ++pass) {
+  __shared__ int redo_flag[2];   // one flag per pass that may ask for another
+  if (tid < 2) redo_flag[tid] = 0;
+  auto run_pass = [&](auto track) __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = f32x16{};
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      l_run[qb] = 0.f;
+      l_run[qb][0] = l_run[qb][1] = 0.f;
       x_max[qb] = -INFINITY;
     }
     const int n_pre = min(kRing, n_tiles);
     for (int t = 0; t < n_pre; ++t) issue(t);
     // tiles 0 and 1 in LDS (K(0), K(1), V(0))
     wait_tiles(n_pre - 1 - min(1, n_tiles - 1));
-    if (pass == 0 && tid == 0) redo_flag = 0;
     __syncthreads();
 
     if (n_tiles > 0) {
@@ -375,8 +380,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
         mask(0, sq[0]);
         mask(0, sq[1]);
       }
-      if (pass == 0) {
-        // reference: the row max of the first tile
+      if (!decltype(track)::value) {
+        // first pass: the reference is the row max of the first tile
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
           float mx = sq[qb][0];
@@ -387,14 +392,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
         }
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) soft_pair(0, j);   // P(0) block 0
+      for (int j = 0; j < 8; ++j) soft_pair(0, j, track);   // P(0) block 0
     }
     // Step t loads tile t + kRing - 1 into the slot of tile t - 1 (free since
     // the barrier that ended step t - 1); step 0 has nothing to load, the
     // prologue filled every slot.
     int t = 0;
     if (t + 2 < n_tiles) {
-      step(0, kOn{}, kOff{}, -1);
+      step(0, kOn{}, kOff{}, -1, track);
       end_of_step(0);
       t = 1;
     }
@@ -403,40 +408,60 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     // for the tile loads in flight) at the top of every iteration
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
     for (; t + kRing < n_tiles; ++t) {      // loads every step, constant wait count
-      step(t, kOn{}, kOff{}, t + kRing - 1);
+      step(t, kOn{}, kOff{}, t + kRing - 1, track);
       end_of_step_steady();
     }
     for (; t + 2 < n_tiles; ++t) {
-      step(t, kOn{}, kOff{}, t + kRing - 1 < n_tiles ? t + kRing - 1 : -1);
+      step(t, kOn{}, kOff{}, t + kRing - 1 < n_tiles ? t + kRing - 1 : -1, track);
       end_of_step(t);
     }
     if (t + 1 < n_tiles) {   // S of the last tile (t + 1), which may be ragged
-      step(t, kOn{}, kOn{}, -1);
+      step(t, kOn{}, kOn{}, -1, track);
       end_of_step(t);
       ++t;
     }
-    if (t < n_tiles) step(t, kOff{}, kOff{}, -1);   // the last tile: PV only
-    if (pass == 1) break;
-    // did any row of the workgroup exceed its reference by more than the headroom?
-    float xm[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x_max[qb]), __float_as_uint(x_max[qb]), false, false);
-      xm[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    }
-    const bool over = xm[0] > kHeadroom || xm[1] > kHeadroom;
-    if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) redo_flag = 1;
+    if (t < n_tiles) step(t, kOff{}, kOff{}, -1, track);   // the last tile: PV only
+  };
+
+  // this lane's rows: row sums (the lanes l and l + 32 hold halves) and x_max
+  auto row_sum = [&](int qb) __attribute__((always_inline)) {
+    const float l_lane = l_run[qb][0] + l_run[qb][1];
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_lane), __float_as_uint(l_lane), false, false);
+    return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  };
+  auto row_xmax = [&](int qb) __attribute__((always_inline)) {
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x_max[qb]), __float_as_uint(x_max[qb]), false, false);
+    return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+  };
+  constexpr float kMaxSum = 18446744073709551616.0f;   // 2^kHeadroom
+  run_pass(kOff{});
+  {
+    const float l0 = row_sum(0), l1 = row_sum(1);
+    const bool over = !(l0 <= kMaxSum) || !(l1 <= kMaxSum);   // also true for inf / NaN
+    if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) redo_flag[0] = 1;
     __syncthreads();
-    if (redo_flag == 0) break;
-    m_ref[0] += xm[0];
-    m_ref[1] += xm[1];
+    if (__builtin_amdgcn_readfirstlane(redo_flag[0]) != 0) {
+      // finite sums: probabilities <= 1 after the shift (l >= 2^x_max)
+      if (l0 > kMaxSum && l0 <= FLT_MAX) m_ref[0] += __log2f(l0);
+      if (l1 > kMaxSum && l1 <= FLT_MAX) m_ref[1] += __log2f(l1);
+      for (int pass = 1;; ++pass) {
+        run_pass(kOn{});
+        if (pass == 2) break;
+        const float xm0 = row_xmax(0), xm1 = row_xmax(1);
+        const bool over2 = xm0 > kHeadroom || xm1 > kHeadroom;
+        if (__builtin_amdgcn_ballot_w64(over2) != 0 && lane == 0) redo_flag[1] = 1;
+        __syncthreads();
+        if (__builtin_amdgcn_readfirstlane(redo_flag[1]) == 0) break;
+        m_ref[0] += xm0;   // the exact row max: every x <= 0
+        m_ref[1] += xm1;
+      }
+    }
   }
 
   // ---- normalise and store
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run[qb]), __float_as_uint(l_run[qb]), false, false);
-    const float l_tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    const float l_tot = row_sum(qb);
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
     if (my_q[qb] < q_end) {
       bf16* op = O + (int64_t)my_q[qb] * os + head * D + 4 * fh;

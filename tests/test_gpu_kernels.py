@@ -189,20 +189,24 @@ def test_attention_varlen(dtype, H, d, lq, lk):
     check(host(out), ref, dtype, "attention")
 
 
-@pytest.mark.parametrize("jump_key", [100, 1999])
-def test_attention_late_score_jump(jump_key):
+@pytest.mark.parametrize("jump_key,big_val", [(100, 20.0), (1999, 20.0), (1500, 10.0)])
+def test_attention_late_score_jump(jump_key, big_val):
     """A key far past the first tile whose score exceeds every earlier one by
-    far more than the kernel's softmax headroom (2^64): the workgroup must
-    detect it and recompute with the exact row max."""
+    far more than the kernel's softmax headroom (2^64).  Key = 20 * ones
+    scores 0.5 * 20 * 128 / sqrt(128) = 113 (163 in log2 units): its
+    probability overflows fp32, the row sum is inf and the exact row max has
+    to be found.  Key = 10 * ones scores 82 in log2 units: the row sum stays
+    finite but above 2^64 and one recomputation with a shifted reference
+    suffices."""
     B = require_gpu()
-    log(f"case attention late score jump key={jump_key}")
+    log(f"case attention late score jump key={jump_key} value={big_val}")
     H, d, n = 2, 128, 2048
     W = H * d
     qkv = synth.draw((n, 3 * W), (33, jump_key), "bf16").copy()
     half = np.float32(0.5).view(np.uint32) >> 16          # bf16 bits of 0.5
-    big = np.float32(20.0).view(np.uint32) >> 16
+    big = np.float32(big_val).view(np.uint32) >> 16
     qkv[:, :W] = half                                      # every query = 0.5 * ones
-    qkv[jump_key, W:2 * W] = big                           # one key = 20 * ones: score ~ +82 (log2 units)
+    qkv[jump_key, W:2 * W] = big                           # one key = big_val * ones
     t = dev(qkv)
     out = empty((n, W), "bf16")
     cu = [0, n]
