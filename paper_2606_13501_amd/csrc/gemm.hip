@@ -33,14 +33,17 @@ constexpr int kRowBytes = BK * 2;                   // 128 B: one full cache lin
 constexpr int kTileBytes = BM * kRowBytes;          // one operand tile of one step (32 KiB)
 constexpr int kStageBytes = 2 * kTileBytes;         // A tile + W tile
 constexpr int kLoads = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave, operand and step (8)
+constexpr int kEpiBytes = 32 * 256;                 // per wave: 32 rows x 64 fp32 (epilogue window)
 constexpr int kGroupM = 4;                          // tile rows per raster group
 constexpr int kXcds = 8;                            // gfx950: 8 XCDs, workgroups dispatched round-robin
 
+// gelu_tanh(z) = z (1 + tanh u) / 2 = z / (1 + e^(-2u)), u = sqrt(2/pi) (z + 0.044715 z^3)
 __device__ __forceinline__ float gelu_tanh(float z) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
   const float k1 = 0.044715f;
-  float u = k0 * (z + k1 * z * z * z);
-  return 0.5f * z * (1.0f + tanhf(u));
+  const float u = k0 * fmaf(k1 * z, z * z, z);
+  const float e = __builtin_amdgcn_exp2f(-2.0f * 1.4426950408889634f * u);   // inf for u << 0: z / inf = 0
+  return z * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 // Logical tile of hardware workgroup b: each XCD gets a contiguous range of
@@ -79,7 +82,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     const bf16* __restrict__ bias, bf16* __restrict__ C, int64_t ldc, const bf16* R, int64_t ldr,
     const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K,
     int tiles_m, int tiles_n) {
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes + kWaves * kEpiBytes];
 
   int tm, tn;
   if (!tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn)) return;
@@ -252,41 +255,74 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     if (s + 1 < KT) step(s + 1, r1, r0, true, false);
   }
 
-  // epilogue: acc[i][j][4g+e] = C[m][n] with m = m0 + wm*128 + 32j + (lane&31),
-  // n = n0 + wn*128 + 32i + 8g + 4*(lane>>5) + e
+  // Epilogue through a wave-private LDS window of 32 rows x 64 columns
+  // (fp32): acc[i][j][4 g + e] = C[m][n] with m = m0 + wm*128 + 32j + fr and
+  // n = n0 + wn*128 + 32i + 8g + 4fh + e.  Each round writes two column
+  // blocks of one row block as the MFMAs left them (a lane: 4 consecutive
+  // columns of one row) and reads them back row-contiguously, so each
+  // global access of a wave covers whole 128-byte row segments.  16-byte
+  // chunk c of window row r sits at physical chunk c ^ (r % 16): both the
+  // writes and the reads are free of bank conflicts.  One wave's LDS
+  // operations complete in order, so the window needs no barrier.
+  char* const ew = smem + kStages * kStageBytes + wave * kEpiBytes;
+  const int er = lane >> 4, ec = lane & 15;   // read role: rows er + 4 k, chunk ec
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int m = m0 + wm * 128 + 32 * j + fr;
-    if (m >= M) continue;
-    const float* g = nullptr;
-    if (EPI == DIT_EPI_GATED_RESIDUAL) g = gate + (int64_t)find_req(req.cu, req.n_req, m) * gate_stride;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int ih = 0; ih < 2; ++ih) {
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        const int n = n0 + wn * 128 + 32 * i + 8 * gq + 4 * fh;
-        if (n >= N) continue;
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const f32x4 v = {acc[2 * ih + ii][j][4 * gq], acc[2 * ih + ii][j][4 * gq + 1],
+                           acc[2 * ih + ii][j][4 * gq + 2], acc[2 * ih + ii][j][4 * gq + 3]};
+          const int c = 8 * ii + 2 * gq + fh;
+          *reinterpret_cast<f32x4*>(ew + fr * 256 + ((c ^ (fr & 15)) << 4)) = v;
+        }
+      // all of a round's loads are issued before its first store: C may
+      // alias R, so no load could be moved above an earlier store
+      const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+      const bool n_ok = n < N;
+      float bsum[4] = {0.f, 0.f, 0.f, 0.f};
+      if (bias && n_ok) {
+        const bf16x4 bv = *reinterpret_cast<const bf16x4*>(bias + n);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bsum[e] = (float)bv[e];
+      }
+      f32x4 zv[8];
+      bf16x4 rv[8];
+      f32x4 gv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int r = 4 * k + er;
+        zv[k] = *reinterpret_cast<const f32x4*>(ew + r * 256 + ((ec ^ (r & 15)) << 4));
+        const int m = m0 + wm * 128 + 32 * j + r;
+        if (EPI == DIT_EPI_RESIDUAL || EPI == DIT_EPI_GATED_RESIDUAL) {
+          rv[k] = bf16x4{};
+          if (m < M && n_ok) rv[k] = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
+        }
+        if (EPI == DIT_EPI_GATED_RESIDUAL) {
+          gv[k] = f32x4{};
+          if (m < M && n_ok)
+            gv[k] = *reinterpret_cast<const f32x4*>(gate + (int64_t)find_req(req.cu, req.n_req, m) * gate_stride + n);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int m = m0 + wm * 128 + 32 * j + 4 * k + er;
+        if (m >= M || !n_ok) continue;
         float z[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) z[e] = acc[i][j][4 * gq + e];
-        if (bias) {
-          bf16x4 bv = *reinterpret_cast<const bf16x4*>(bias + n);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] += (float)bv[e];
-        }
+        for (int e = 0; e < 4; ++e) z[e] = zv[k][e] + bsum[e];
         if (EPI == DIT_EPI_GELU_TANH) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) z[e] = gelu_tanh(z[e]);
-        } else if (EPI == DIT_EPI_RESIDUAL || EPI == DIT_EPI_GATED_RESIDUAL) {
-          bf16x4 rv = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
-          if (EPI == DIT_EPI_GATED_RESIDUAL) {
-            f32x4 gv = *reinterpret_cast<const f32x4*>(g + n);
+        } else if (EPI == DIT_EPI_GATED_RESIDUAL) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) z[e] = (float)rv[e] + gv[e] * z[e];
-          } else {
+          for (int e = 0; e < 4; ++e) z[e] = (float)rv[k][e] + gv[k][e] * z[e];
+        } else if (EPI == DIT_EPI_RESIDUAL) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) z[e] = (float)rv[e] + z[e];
-          }
+          for (int e = 0; e < 4; ++e) z[e] = (float)rv[k][e] + z[e];
         }
         bf16x4 o;
 #pragma unroll
