@@ -46,21 +46,38 @@ __device__ __forceinline__ float gelu_tanh(float z) {
   return z * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// Logical tile of hardware workgroup b: each XCD gets a contiguous range of
-// logical tiles, and tiles are rastered in groups of kGroupM tile rows so the
-// workgroups resident on one XCD share A and W panels in its L2.
-__device__ __forceinline__ bool tile_of(int b, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
-  int per_xcd = nb / kXcds;
-  int t = (b % kXcds) * per_xcd + b / kXcds;
-  if (t >= tiles_m * tiles_n) return false;
-  int width = kGroupM * tiles_n;
-  int group = t / width;
-  int first_m = group * kGroupM;
-  int gsize = min(tiles_m - first_m, kGroupM);
-  int r = t - group * width;
-  tm = first_m + r % gsize;
-  tn = r / gsize;
-  return true;
+// Tile sequence of a workgroup.  Each XCD owns a contiguous range of logical
+// tiles (the dispatcher places workgroup b on XCD b mod 8); the workgroups of
+// one XCD take its tiles round-robin, so at any time they work on adjacent
+// tiles.  Logical tiles are rastered in groups of kGroupM tile rows, so the
+// tiles resident on one XCD share A and W panels in its L2.
+struct TileSeq {
+  int first, stride, count;   // logical tiles first + stride * it, it < count
+  int tiles_m, tiles_n;
+  __device__ void coords(int it, int& tm, int& tn) const {
+    const int t = first + stride * it;
+    const int width = kGroupM * tiles_n;
+    const int group = t / width;
+    const int first_m = group * kGroupM;
+    const int gsize = min(tiles_m - first_m, kGroupM);
+    const int r = t - group * width;
+    tm = first_m + r % gsize;
+    tn = r / gsize;
+  }
+};
+
+__device__ __forceinline__ TileSeq tile_seq(int b, int nb, int tiles_m, int tiles_n) {
+  const int tiles = tiles_m * tiles_n;
+  const int per_xcd = (tiles + kXcds - 1) / kXcds;
+  const int x = b % kXcds, slot = b / kXcds, wgs = nb / kXcds;
+  const int lo = x * per_xcd, hi = min(tiles, lo + per_xcd);
+  TileSeq q;
+  q.first = lo + slot;
+  q.stride = wgs;
+  q.count = q.first < hi ? (hi - q.first + wgs - 1) / wgs : 0;
+  q.tiles_m = tiles_m;
+  q.tiles_n = tiles_n;
+  return q;
 }
 
 // 16-byte chunk swizzle of a 128-byte LDS row: a fragment read touches 16
@@ -76,7 +93,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
-template <int EPI>
+// The same descriptor as a plain vector (operand of the LDS-direct load).
+__device__ __forceinline__ u32x4 make_desc(const void* base, int64_t bytes) {
+  const uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
+  const uint64_t p = (uint64_t)base;
+  return u32x4{(uint32_t)p, (uint32_t)(p >> 32) & 0xFFFFu, n, 0x00020000u};
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane i writes LDS
+// bytes lds + 16 i .. +15.  Inline assembly, so the compiler does not make
+// later LDS reads wait for it; completion is waited for by hand.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_lds16(const u32x4& desc, int voff, int soff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "m0");
+}
+#pragma clang diagnostic pop
+
+// SEQ: the workgroup runs a sequence of tiles (K / 64 even and >= 6);
+// otherwise one tile per workgroup and any K / 64.
+template <int EPI, bool SEQ>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     const bf16* __restrict__ A, int64_t lda, const bf16* __restrict__ W, int64_t ldw,
     const bf16* __restrict__ bias, bf16* __restrict__ C, int64_t ldc, const bf16* R, int64_t ldr,
@@ -84,9 +121,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     int tiles_m, int tiles_n) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes + kWaves * kEpiBytes];
 
+  const TileSeq seq = tile_seq(blockIdx.x, gridDim.x, tiles_m, tiles_n);
+  if (seq.count == 0) return;
   int tm, tn;
-  if (!tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn)) return;
-  const int m0 = tm * BM, n0 = tn * BN;
+  seq.coords(0, tm, tn);
+  int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -97,24 +136,27 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // of W.  Lane i of piece q holds row 8 q + i / 8, logical chunk
   // (i % 8) ^ row_swizzle(row), and stores it at LDS byte q * 1024 + 16 i,
   // i.e. physical chunk i % 8 of that row.
-  const auto a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
-  const auto w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
-  int a_voff[kLoads], w_voff[kLoads];
+  auto a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
+  auto w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
+  // Row 8 q + i / 8 has row_swizzle = 4 (q % 2) + i / 16, so the lane part of
+  // a load's offset takes one of two values per operand (by the parity of q)
+  // and the rest, 8 q rows, is uniform (the scalar offset of the load).
+  int a_vo[2], w_vo[2];
 #pragma unroll
-  for (int u = 0; u < kLoads; ++u) {
-    const int q = kLoads * wave + u;
-    const int r = 8 * q + (lane >> 3);
-    const int c = (lane & 7) ^ row_swizzle(r);
-    a_voff[u] = r * (int)lda * 2 + c * 16;
-    w_voff[u] = r * (int)ldw * 2 + c * 16;
+  for (int par = 0; par < 2; ++par) {
+    const int c = (lane & 7) ^ (4 * par + (lane >> 4));
+    a_vo[par] = (lane >> 3) * (int)lda * 2 + c * 16;
+    w_vo[par] = (lane >> 3) * (int)ldw * 2 + c * 16;
   }
+  auto a_so = [&](int u) { return (kLoads * wave + u) * 16 * (int)lda; };   // 8 q rows, in bytes
+  auto w_so = [&](int u) { return (kLoads * wave + u) * 16 * (int)ldw; };
   struct Stage { u32x4 a[kLoads], w[kLoads]; };   // one step of this wave's pieces
   auto gload = [&](Stage& r, int step) {
     const int soff = step * BK * 2;
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      r.a[u] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_voff[u], soff, 0);
-      r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_voff[u], soff, 0);
+      r.a[u] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[u & 1], soff + a_so(u), 0);
+      r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[u & 1], soff + w_so(u), 0);
     }
   };
   auto sstore = [&](const Stage& r, int step) {
@@ -178,17 +220,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   };
   // items u0 .. u0 + 3 of a register stage (items 0-7: A pieces, 8-15: W
   // pieces): store each into the LDS slot of step st_step, then reload it
-  // with step ld_step (skipped past the last step when `guard`)
-  auto io4 = [&](Stage& R, int u0, int st_step, int ld_step, bool guard) {
+  // with step ld_step (each part only when asked for)
+  auto io4 = [&](Stage& R, int u0, int st_step, int ld_step, bool do_store, bool do_load) {
     char* st = smem + (st_step % kStages) * kStageBytes + kLoads * wave * 1024 + lane * 16;
     const int soff = ld_step * BK * 2;
 #pragma unroll
     for (int u = u0; u < u0 + 4; ++u) {
       const int p = u & 7;
       u32x4& v = u < 8 ? R.a[p] : R.w[p];
-      if (!guard || st_step < KT) *reinterpret_cast<u32x4*>(st + (u < 8 ? 0 : kTileBytes) + p * 1024) = v;
-      if (!guard || ld_step < KT)
-        v = __builtin_amdgcn_raw_buffer_load_b128(u < 8 ? a_rs : w_rs, u < 8 ? a_voff[p] : w_voff[p], soff, 0);
+      if (do_store) *reinterpret_cast<u32x4*>(st + (u < 8 ? 0 : kTileBytes) + p * 1024) = v;
+      if (do_load)
+        v = u < 8 ? __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[p & 1], soff + a_so(p), 0)
+                  : __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[p & 1], soff + w_so(p), 0);
     }
   };
 
@@ -206,54 +249,104 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   //   read q3 -> f1 | MFMAs f0 | P items 12-15
   //   barrier
   //   read q0 of s + 1 -> f0 | MFMAs f1 | Q items 0-3  (store s + 2, load s + 4)
+  // A workgroup runs a sequence of tiles.  The two LDS slots of a tile's
+  // last two steps are free after their mid-step barriers; the next tile's
+  // steps 0 and 1 are loaded straight into them from there (LDS-direct
+  // loads), so that tile starts without waiting for memory.  The last steps
+  // load nothing into the register stages, which are therefore free during
+  // the epilogue.  (With an odd step count the host gives every workgroup a
+  // single tile.)
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+  u32x4 nad{}, nwd{};   // the next tile's A and W
+  bool has_next = false;
+  auto dma_step = [&](int step) {   // step 0 or 1 of the next tile into slot `step`
+    const uint32_t st = lds_base + step * kStageBytes + kLoads * wave * 1024;
+    const int soff = step * BK * 2;
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) {
+      load_lds16(nad, a_vo[u & 1], soff + a_so(u), st + u * 1024);
+      load_lds16(nwd, w_vo[u & 1], soff + w_so(u), st + kTileBytes + u * 1024);
+    }
+  };
   Stage r0, r1;
-  // prologue: slots 0 and 1 hold steps 0 and 1, r0 / r1 carry steps 2 / 3
+  Frags f0, f1;
+  // Step s: P drains step s + 1 (stP) and reloads with s + 3 (ldP), Q drains
+  // step s + 2 (stQ) and reloads with s + 4 (ldQ); `dma` >= 0 loads step dma
+  // of the next tile into slot dma after the barrier.  At the call sites the
+  // flags are constants wherever possible, so the compiler knows exactly
+  // which loads are in flight and derives exact wait counts.
+  auto step = [&](int s, Stage& P, Stage& Q, bool first, bool stP, bool ldP, bool stQ, bool ldQ, int dma) {
+    read(f1, s, 1);
+    mma(f0);
+    if (!first) io4(P, 4, s + 1, s + 3, stP, ldP);
+    pattern();
+    read(f0, s, 2);
+    mma(f1);
+    if (!first) io4(P, 8, s + 1, s + 3, stP, ldP);
+    pattern();
+    read(f1, s, 3);
+    mma(f0);
+    if (!first) io4(P, 12, s + 1, s + 3, stP, ldP);
+    pattern();
+    __syncthreads();
+    if (dma >= 0) dma_step(dma);
+    read(f0, s + 1, 0);   // after the last step: a harmless read of the idle slot
+    mma(f1);
+    io4(Q, 0, s + 2, s + 4, stQ, ldQ);
+    pattern();
+  };
+  // first tile: slots 0 and 1 get steps 0 and 1 through the register stages
   // (steps past the end load zeros or bytes of later rows; they fill slots
   // and registers that are never consumed)
   gload(r0, 0);
   gload(r1, 1);
   sstore(r0, 0);
   sstore(r1, 1);
-  // keep the two register stages' loads in this order (as in the loop), so
-  // the wait counts the compiler derives inside the loop stay exact
-  __builtin_amdgcn_sched_barrier(0);
-  gload(r0, 2);
-  __builtin_amdgcn_sched_barrier(0);
-  gload(r1, 3);
-  __builtin_amdgcn_sched_barrier(0);
-  __syncthreads();
-  Frags f0, f1;
-  read(f0, 0, 0);
-
-  auto step = [&](int s, Stage& P, Stage& Q, bool guard, bool first) {
-    read(f1, s, 1);
-    mma(f0);
-    if (!first) io4(P, 4, s + 1, s + 3, guard);
-    pattern();
-    read(f0, s, 2);
-    mma(f1);
-    if (!first) io4(P, 8, s + 1, s + 3, guard);
-    pattern();
-    read(f1, s, 3);
-    mma(f0);
-    if (!first) io4(P, 12, s + 1, s + 3, guard);
-    pattern();
+  for (int it = 0;; ++it) {
+    has_next = SEQ && it + 1 < seq.count;
+    int tm1 = 0, tn1 = 0;
+    if (has_next) {
+      seq.coords(it + 1, tm1, tn1);
+      nad = make_desc(A + (int64_t)tm1 * BM * lda, ((int64_t)(M - tm1 * BM - 1) * lda + K) * 2);
+      nwd = make_desc(W + (int64_t)tn1 * BN * ldw, ((int64_t)(N - tn1 * BN - 1) * ldw + K) * 2);
+    }
+    // r0 / r1 carry steps 2 / 3; keep the two register stages' loads in this
+    // order (as in the loop), so the wait counts the compiler derives inside
+    // the loop stay exact
+    __builtin_amdgcn_sched_barrier(0);
+    gload(r0, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    gload(r1, 3);
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    read(f0, s + 1, 0);   // after the last step: a harmless read of the idle slot
-    mma(f1);
-    io4(Q, 0, s + 2, s + 4, guard);
-    pattern();
-  };
-  step(0, r1, r0, true, true);   // window -1 (step 1 into slot 1) was the prologue
-  int s = 1;
-  for (; s + 5 < KT; s += 2) {
-    step(s, r0, r1, false, false);
-    step(s + 1, r1, r0, false, false);
-  }
-  for (; s < KT; s += 2) {
-    step(s, r0, r1, true, false);
-    if (s + 1 < KT) step(s + 1, r1, r0, true, false);
-  }
+    read(f0, 0, 0);
+    // an even step uses (P, Q) = (r1, r0), an odd one (r0, r1); window -1
+    // (step 1 into slot 1) is already in LDS
+    if constexpr (SEQ) {
+      step(0, r1, r0, true, false, false, true, true, -1);
+      // nothing issued before this point may be pending when the loop starts:
+      // the wait counts the compiler derives inside it are then exact (else
+      // a merge at its header can put a full wait into every iteration)
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+      int s = 1;
+      for (; s + 5 < KT; s += 2) {
+        step(s, r0, r1, false, true, true, true, true, -1);
+        step(s + 1, r1, r0, false, true, true, true, true, -1);
+      }
+      // s = KT - 5: the last five steps, loads stop at step KT - 1
+      step(s, r0, r1, false, true, true, true, true, -1);
+      step(s + 1, r1, r0, false, true, true, true, false, -1);
+      step(s + 2, r0, r1, false, true, false, true, false, -1);
+      step(s + 3, r1, r0, false, true, false, false, false, has_next ? 0 : -1);
+      step(s + 4, r0, r1, false, false, false, false, false, has_next ? 1 : -1);
+    } else {   // any step count, a single tile
+      step(0, r1, r0, true, false, false, 2 < KT, 4 < KT, -1);
+      for (int s = 1; s < KT; s += 2) {
+        step(s, r0, r1, false, s + 1 < KT, s + 3 < KT, s + 2 < KT, s + 4 < KT, -1);
+        if (s + 1 < KT) step(s + 1, r1, r0, false, s + 2 < KT, s + 4 < KT, s + 3 < KT, s + 5 < KT, -1);
+      }
+    }
+    if (has_next) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the next tile's steps 0 and 1
 
   // Epilogue through a wave-private LDS window of 32 rows x 64 columns
   // (fp32): acc[i][j][4 g + e] = C[m][n] with m = m0 + wm*128 + 32j + fr and
@@ -264,72 +357,113 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // chunk c of window row r sits at physical chunk c ^ (r % 16): both the
   // writes and the reads are free of bank conflicts.  One wave's LDS
   // operations complete in order, so the window needs no barrier.
+  // The residual rows of two row blocks (and the gate row of each block,
+  // when all its rows belong to one request) are loaded before any of their
+  // outputs is computed, so the epilogue waits for memory twice per tile;
+  // the register stages are free here.  C may alias R: every element is
+  // read before it is written, by the same lane.
   char* const ew = smem + kStages * kStageBytes + wave * kEpiBytes;
   const int er = lane >> 4, ec = lane & 15;   // read role: rows er + 4 k, chunk ec
+  float bsum[2][4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int ih = 0; ih < 2; ++ih) {
+    const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
 #pragma unroll
-    for (int ih = 0; ih < 2; ++ih) {
+    for (int e = 0; e < 4; ++e) bsum[ih][e] = 0.f;
+    if (bias && n < N) {
+      const bf16x4 bv = *reinterpret_cast<const bf16x4*>(bias + n);
 #pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
+      for (int e = 0; e < 4; ++e) bsum[ih][e] = (float)bv[e];
+    }
+  }
 #pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-          const f32x4 v = {acc[2 * ih + ii][j][4 * gq], acc[2 * ih + ii][j][4 * gq + 1],
-                           acc[2 * ih + ii][j][4 * gq + 2], acc[2 * ih + ii][j][4 * gq + 3]};
-          const int c = 8 * ii + 2 * gq + fh;
-          *reinterpret_cast<f32x4*>(ew + fr * 256 + ((c ^ (fr & 15)) << 4)) = v;
-        }
-      // all of a round's loads are issued before its first store: C may
-      // alias R, so no load could be moved above an earlier store
-      const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
-      const bool n_ok = n < N;
-      float bsum[4] = {0.f, 0.f, 0.f, 0.f};
-      if (bias && n_ok) {
-        const bf16x4 bv = *reinterpret_cast<const bf16x4*>(bias + n);
+  for (int hj = 0; hj < 2; ++hj) {
+    constexpr bool kRes = EPI == DIT_EPI_RESIDUAL || EPI == DIT_EPI_GATED_RESIDUAL;
+    bf16x4 rv[2][2][8];
+    f32x4 gv[2][2];
+    bool g_one[2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) bsum[e] = (float)bv[e];
-      }
-      f32x4 zv[8];
-      bf16x4 rv[8];
-      f32x4 gv[8];
+    for (int jj = 0; jj < 2; ++jj) {
+      const int mb = m0 + wm * 128 + 32 * (2 * hj + jj);   // first row of the block
+      if (EPI == DIT_EPI_GATED_RESIDUAL) {
+        const int r_lo = find_req(req.cu, req.n_req, min(mb, M - 1));
+        const int r_hi = find_req(req.cu, req.n_req, min(mb + 31, M - 1));
+        g_one[jj] = r_lo == r_hi;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int r = 4 * k + er;
-        zv[k] = *reinterpret_cast<const f32x4*>(ew + r * 256 + ((ec ^ (r & 15)) << 4));
-        const int m = m0 + wm * 128 + 32 * j + r;
-        if (EPI == DIT_EPI_RESIDUAL || EPI == DIT_EPI_GATED_RESIDUAL) {
-          rv[k] = bf16x4{};
-          if (m < M && n_ok) rv[k] = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
-        }
-        if (EPI == DIT_EPI_GATED_RESIDUAL) {
-          gv[k] = f32x4{};
-          if (m < M && n_ok)
-            gv[k] = *reinterpret_cast<const f32x4*>(gate + (int64_t)find_req(req.cu, req.n_req, m) * gate_stride + n);
+        for (int ih = 0; ih < 2; ++ih) {
+          const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+          gv[jj][ih] = f32x4{};
+          if (g_one[jj] && n < N) gv[jj][ih] = *reinterpret_cast<const f32x4*>(gate + (int64_t)r_lo * gate_stride + n);
         }
       }
+      if (kRes) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int m = m0 + wm * 128 + 32 * j + 4 * k + er;
-        if (m >= M || !n_ok) continue;
-        float z[4];
+        for (int ih = 0; ih < 2; ++ih) {
+          const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) z[e] = zv[k][e] + bsum[e];
-        if (EPI == DIT_EPI_GELU_TANH) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] = gelu_tanh(z[e]);
-        } else if (EPI == DIT_EPI_GATED_RESIDUAL) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] = (float)rv[k][e] + gv[k][e] * z[e];
-        } else if (EPI == DIT_EPI_RESIDUAL) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] = (float)rv[k][e] + z[e];
+          for (int k = 0; k < 8; ++k) {
+            const int m = mb + 4 * k + er;
+            rv[jj][ih][k] = bf16x4{};
+            if (m < M && n < N) rv[jj][ih][k] = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
+          }
         }
-        bf16x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (bf16)z[e];
-        *reinterpret_cast<bf16x4*>(C + (int64_t)m * ldc + n) = o;
       }
     }
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int j = 2 * hj + jj;
+#pragma unroll
+      for (int ih = 0; ih < 2; ++ih) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            const f32x4 v = {acc[2 * ih + ii][j][4 * gq], acc[2 * ih + ii][j][4 * gq + 1],
+                             acc[2 * ih + ii][j][4 * gq + 2], acc[2 * ih + ii][j][4 * gq + 3]};
+            const int c = 8 * ii + 2 * gq + fh;
+            *reinterpret_cast<f32x4*>(ew + fr * 256 + ((c ^ (fr & 15)) << 4)) = v;
+          }
+        const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+        if (n >= N) continue;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int r = 4 * k + er;
+          const f32x4 zv = *reinterpret_cast<const f32x4*>(ew + r * 256 + ((ec ^ (r & 15)) << 4));
+          const int m = m0 + wm * 128 + 32 * j + r;
+          if (m >= M) continue;
+          float z[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[e] = zv[e] + bsum[ih][e];
+          if (EPI == DIT_EPI_GELU_TANH) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[e] = gelu_tanh(z[e]);
+          } else if (EPI == DIT_EPI_GATED_RESIDUAL) {
+            f32x4 g4 = gv[jj][ih];
+            if (!g_one[jj])   // the block spans a request boundary
+              g4 = *reinterpret_cast<const f32x4*>(gate + (int64_t)find_req(req.cu, req.n_req, m) * gate_stride + n);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[e] = (float)rv[jj][ih][k][e] + g4[e] * z[e];
+          } else if (EPI == DIT_EPI_RESIDUAL) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[e] = (float)rv[jj][ih][k][e] + z[e];
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = (bf16)z[e];
+          *reinterpret_cast<bf16x4*>(C + (int64_t)m * ldc + n) = o;
+        }
+      }
+    }
+  }
+    if (!has_next) break;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    m0 = tm1 * BM;
+    n0 = tn1 * BN;
+    a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
+    w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
   }
 }
 
@@ -390,15 +524,38 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(
   }
 }
 
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 template <int EPI>
 hipError_t launch_bf16(const LinearArgs& p, hipStream_t s) {
   int tiles_m = (int)((p.M + BM - 1) / BM);
   int tiles_n = (p.N + BN - 1) / BN;
   int tiles = tiles_m * tiles_n;
-  int grid = (tiles + kXcds - 1) / kXcds * kXcds;
-  gemm_bf16_nt<EPI><<<grid, kThreads, 0, s>>>(
-      (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
-      (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n);
+  int grid = (tiles + kXcds - 1) / kXcds * kXcds;   // one tile per workgroup
+  const int kt = p.K / BK;
+  if (kt % 2 == 0 && kt >= 6) {
+    // one workgroup per compute unit, each running a sequence of tiles
+    const int resident = cu_count() / kXcds * kXcds;
+    if (resident >= kXcds && grid > resident) grid = resident;
+    gemm_bf16_nt<EPI, true><<<grid, kThreads, 0, s>>>(
+        (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
+        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n);
+  } else {
+    gemm_bf16_nt<EPI, false><<<grid, kThreads, 0, s>>>(
+        (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
+        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n);
+  }
   return hipGetLastError();
 }
 

@@ -95,6 +95,36 @@ def test_linear(dtype, M, N, K, lengths, epi):
     check(host(out), z, dtype, f"linear epi={epi}")
 
 
+@pytest.mark.parametrize("epi", [0, 1, 3])
+def test_linear_tile_sequences(epi):
+    """More output tiles (49 x 12 = 588, ragged in M and N) than compute units:
+    each workgroup runs a sequence of 2 or 3 tiles and loads the next tile's
+    first K steps while finishing the current one.  Checked on sampled rows
+    covering the first, middle and last row of every tile row."""
+    B = require_gpu()
+    M, N, K, lengths = 12288 + 77, 2816 + 64, 768, [5000, 7365]
+    log(f"case linear tile sequences M={M} N={N} K={K} epi={epi}")
+    cu = _cu(lengths)
+    a = synth.draw((M, K), (15, M, N, K), "bf16")
+    w = synth.draw((N, K), (16, M, N, K), "bf16", std=0.02)
+    b = synth.draw((N,), (17, M, N, K), "bf16", std=0.02)
+    res = synth.draw((M, N), (18, M, N, K), "bf16")
+    gate = synth.draw((len(lengths), N), (19, M, N, K), "f32", std=0.7)
+    out = empty((M, N), "bf16")
+    B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
+             gate=dev(gate) if epi == 3 else None, gate_stride=N, cu_seqlens=cu if epi == 3 else None)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(0, M, 256), np.minimum(np.arange(0, M, 256) + 128, M - 1),
+                                     np.minimum(np.arange(0, M, 256) + 255, M - 1), [M - 1],
+                                     np.random.default_rng(7).integers(0, M, 200)]))
+    z = O.linear(O.decode(a[rows]), O.decode(w), O.decode(b))
+    if epi == 1:
+        z = O.gelu_tanh(z)
+    elif epi == 3:
+        z = O.decode(res[rows]) + gate[_req_of(cu)[rows]].astype(np.float64) * z
+    check(host(out)[rows], z, "bf16", f"linear tile sequences epi={epi}")
+
+
 def test_linear_inplace_residual():
     """res == out (the block updates x1 in place)."""
     B = require_gpu()
