@@ -324,10 +324,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     // (step 1 into slot 1) is already in LDS
     if constexpr (SEQ) {
       step(0, r1, r0, true, false, false, true, true, -1);
-      // nothing issued before this point may be pending when the loop starts:
-      // the wait counts the compiler derives inside it are then exact (else
-      // a merge at its header can put a full wait into every iteration)
-      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
       int s = 1;
       for (; s + 5 < KT; s += 2) {
         step(s, r0, r1, false, true, true, true, true, -1);
