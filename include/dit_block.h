@@ -207,6 +207,90 @@ dit_status dit_gated_residual(const void *x, const void *z, const void *bias, co
                               int64_t gate_stride, const int32_t *cu_seqlens, int n_req,
                               int hidden, void *out, dit_dtype dtype, hipStream_t stream);
 
+/* ------------------------------------------------------ one denoising step */
+
+/* One denoising step is the unit the paper schedules as a trajectory task: it
+ * advances a request's latent along its diffusion trajectory by one timestep
+ * and leaves a complete latent state behind (section 2.1, Rescheduling
+ * Boundaries; section 3.1, Reschedulable Trajectory Tasks).  The paper does
+ * not define the model, so this is the standard DiT stack around the block:
+ * patch embedding of the latent, a timestep MLP shared by all blocks, B blocks
+ * with per-block adaLN-Zero modulation, an adaLN output layer and a
+ * flow-matching Euler update.  The text keys and values of every block's
+ * cross-attention do not depend on the latent or the timestep, so they are
+ * computed once per request (dit_text_kv) and reused by every step.
+ *
+ * Latent of request r: fp32, channel-major [C, F*pt, H*ph, W*pw] where
+ * (F, H, W) = vl->grid_fhw[r] is its token grid, stored contiguously; the
+ * requests follow each other in order (request r starts after the
+ * C*F*pt*H*ph*W*pw values of requests 0..r-1).  Token n = (f*H + h)*W + w of
+ * the request covers the latent patch at (f*pt, h*ph, w*pw); its patch vector
+ * has P = C*pt*ph*pw entries in the order (c, i, j, k) with i over time,
+ * j over height and k over width, and the model's output uses the same order,
+ * so unpatchify is the exact inverse of patchify.  The step needs whole
+ * requests: cu_seqlens[r+1] - cu_seqlens[r] = F*H*W and pos_offset NULL or 0. */
+typedef struct {
+  dit_block_config block; /* shared by every block */
+  int n_blocks;           /* B >= 1 */
+  int in_channels;        /* C: latent channels (the velocity has the same) */
+  int patch[3];           /* (pt, ph, pw) >= 1; bf16 needs P % 64 == 0, fp32 P % 4 == 0 */
+} dit_model_config;
+
+/* Device pointers (dtype of the config) except `blocks`, a HOST array of
+ * n_blocks block weight sets.  Shapes with P = C*pt*ph*pw: w_t1 [D,F] b_t1 [D]
+ * w_t2 [D,D] b_t2 [D] (the shared timestep MLP); w_pe [D,P] b_pe [D] (patch
+ * embedding); w_hmod [2D,D] b_hmod [2D] (output adaLN: shift, scale);
+ * w_out [P,D] b_out [P] (output projection).  The blocks' own w_t1..b_t2 are
+ * not read: every block takes its modulation W_ada SiLU(c) + b_ada from the
+ * shared c. */
+typedef struct {
+  const void *w_t1, *b_t1, *w_t2, *b_t2;
+  const void *w_pe, *b_pe;
+  const void *w_hmod, *b_hmod;
+  const void *w_out, *b_out;
+  const dit_block_weights *blocks;
+} dit_model_weights;
+
+/* Elements (not bytes) of the text key/value cache: n_blocks * txt_rows * 2D,
+ * dtype of the config.  0 if the arguments are invalid. */
+size_t dit_text_kv_elems(const dit_model_config *cfg, const dit_varlen *vl);
+
+/* The cross-attention keys and values of every block: for block b,
+ * kv[b] = [RMSNorm_heads(txt W_ck^T + b_ck) | txt W_cv^T + b_cv] (the norm only
+ * with qk_norm), [txt_rows, 2D] at kv + b*txt_rows*2D.  txt: [txt_rows, D]. */
+dit_status dit_text_kv(const dit_model_config *cfg, const dit_model_weights *w,
+                       const dit_varlen *vl, const void *txt, void *kv,
+                       hipStream_t stream);
+
+/* Bytes of device workspace dit_denoise_step needs (0 if invalid). */
+size_t dit_denoise_workspace_size(const dit_model_config *cfg, const dit_varlen *vl);
+
+/* One flow-matching Euler step of every request in the batch:
+ *   x   = patchify(latent) W_pe^T + b_pe                    [rows, D]
+ *   c   = W_t2 SiLU(W_t1 emb(t) + b_t1) + b_t2              per request
+ *   x   = Block_b(x; c, kv[b]) for b = 0..B-1
+ *   v   = (LN(x)(1 + scale) + shift) W_out^T + b_out, (shift, scale) = W_hmod SiLU(c) + b_hmod
+ *   latent_out = latent + dt[r] * unpatchify(v)
+ * t, dt: device fp32 [n_req] (timestep given to the model, and the step of
+ * the flow time, sigma_next - sigma; negative when denoising).  latent,
+ * latent_out: fp32 as described above; latent_out may equal latent.  kv: the
+ * cache from dit_text_kv.  Workspace as for dit_block_forward, sized by
+ * dit_denoise_workspace_size. */
+dit_status dit_denoise_step(const dit_model_config *cfg, const dit_model_weights *w,
+                            const dit_varlen *vl, const float *latent, const float *t,
+                            const float *dt, const void *kv, float *latent_out, void *ws,
+                            size_t ws_bytes, hipStream_t stream);
+
+/* The latent <-> token steps of dit_denoise_step on their own.
+ * dit_patchify: tokens [rows, P] (dtype, rounded to nearest even for bf16)
+ * from the fp32 latent.  dit_unpatchify_euler: latent_out = latent +
+ * dt[r] * unpatchify(v), v [rows, P] (dtype); latent_out may equal latent. */
+dit_status dit_patchify(const dit_model_config *cfg, const dit_varlen *vl, const float *latent,
+                        void *tokens, hipStream_t stream);
+dit_status dit_unpatchify_euler(const dit_model_config *cfg, const dit_varlen *vl,
+                                const float *latent, const void *v, const float *dt,
+                                float *latent_out, hipStream_t stream);
+
 /* -------------------------------------------------------------- diagnostics */
 
 const char *dit_status_string(dit_status s);

@@ -63,6 +63,18 @@ class CVarlen(ctypes.Structure):
     ]
 
 
+MODEL_FIELDS = ("w_t1", "b_t1", "w_t2", "b_t2", "w_pe", "b_pe", "w_hmod", "b_hmod", "w_out", "b_out")
+
+
+class CModelConfig(ctypes.Structure):
+    _fields_ = [("block", CConfig), ("n_blocks", ctypes.c_int), ("in_channels", ctypes.c_int),
+                ("patch", ctypes.c_int * 3)]
+
+
+class CModelWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in MODEL_FIELDS] + [("blocks", ctypes.POINTER(CWeights))]
+
+
 _lib = None
 
 
@@ -77,6 +89,7 @@ def lib() -> ctypes.CDLL:
     vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
     PC, PW, PV = ctypes.POINTER(CConfig), ctypes.POINTER(CWeights), ctypes.POINTER(CVarlen)
     PI = ctypes.POINTER(ctypes.c_int32)
+    PM, PMW = ctypes.POINTER(CModelConfig), ctypes.POINTER(CModelWeights)
     sig = {
         "dit_block_workspace_size": (sz, [PC, PV]),
         "dit_block_forward": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
@@ -89,6 +102,12 @@ def lib() -> ctypes.CDLL:
         "dit_linear": (i32, [vp, i64, vp, i64, vp, vp, i64, i64, i32, i32, i32, vp, i64, vp, i64, PI, i32, i32, vp]),
         "dit_qk_norm_rope": (i32, [vp, vp, i64, i64, i32, i32, vp, vp, f32, PI, f32, PV, i32, vp]),
         "dit_gated_residual": (i32, [vp, vp, vp, vp, i64, PI, i32, i32, vp, i32, vp]),
+        "dit_text_kv_elems": (sz, [PM, PV]),
+        "dit_text_kv": (i32, [PM, PMW, PV, vp, vp, vp]),
+        "dit_denoise_workspace_size": (sz, [PM, PV]),
+        "dit_denoise_step": (i32, [PM, PMW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_patchify": (i32, [PM, PV, vp, vp, vp]),
+        "dit_unpatchify_euler": (i32, [PM, PV, vp, vp, vp, vp, vp]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -105,7 +124,9 @@ def exported_symbols() -> Sequence[str]:
     return [n for n in ("dit_block_workspace_size", "dit_block_forward", "dit_block_pre_attention",
                         "dit_block_post_attention", "dit_timestep_modulation", "dit_attention_varlen",
                         "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
-                        "dit_gated_residual", "dit_status_string", "dit_last_error", "dit_abi_version")]
+                        "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
+                        "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_status_string",
+                        "dit_last_error", "dit_abi_version")]
 
 
 def _check(status: int, func: str):
@@ -257,3 +278,59 @@ def gated_residual(x, z, bias, gate, gate_stride, cu_seqlens, out, stream=None):
     _check(lib().dit_gated_residual(_ptr(x), _ptr(z), _ptr(bias), _ptr(gate), gate_stride, _pi(cu), len(cu) - 1,
                                     x.shape[-1], _ptr(out), dtype_code(x.dtype), _stream(stream)),
            "dit_gated_residual")
+
+
+# ------------------------------------------------------- the denoising step
+
+
+class ModelConfig:
+    """Python view of dit_model_config."""
+
+    def __init__(self, block: BlockConfig, n_blocks: int, in_channels: int, patch):
+        self.block = block
+        self.c = CModelConfig()
+        self.c.block = block.c
+        self.c.n_blocks, self.c.in_channels = int(n_blocks), int(in_channels)
+        for i in range(3):
+            self.c.patch[i] = int(patch[i])
+
+
+class ModelWeights:
+    """Python view of dit_model_weights; keeps the host array of block weights alive."""
+
+    def __init__(self, w: Dict[str, Optional[torch.Tensor]], blocks: Sequence[CWeights]):
+        self.blocks = (CWeights * len(blocks))(*blocks)
+        self.c = CModelWeights()
+        for n in MODEL_FIELDS:
+            t = w.get(n)
+            setattr(self.c, n, t.data_ptr() if t is not None else None)
+        self.c.blocks = ctypes.cast(self.blocks, ctypes.POINTER(CWeights))
+
+
+def text_kv_elems(cfg: ModelConfig, vl: Varlen) -> int:
+    return int(lib().dit_text_kv_elems(ctypes.byref(cfg.c), ctypes.byref(vl.c)))
+
+
+def text_kv(cfg: ModelConfig, w: ModelWeights, vl: Varlen, txt, kv, stream=None):
+    _check(lib().dit_text_kv(ctypes.byref(cfg.c), ctypes.byref(w.c), ctypes.byref(vl.c), _ptr(txt), _ptr(kv),
+                             _stream(stream)), "dit_text_kv")
+
+
+def denoise_workspace_size(cfg: ModelConfig, vl: Varlen) -> int:
+    return int(lib().dit_denoise_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c)))
+
+
+def denoise_step(cfg: ModelConfig, w: ModelWeights, vl: Varlen, latent, t, dt, kv, latent_out, ws, stream=None):
+    _check(lib().dit_denoise_step(ctypes.byref(cfg.c), ctypes.byref(w.c), ctypes.byref(vl.c), _ptr(latent), _ptr(t),
+                                  _ptr(dt), _ptr(kv), _ptr(latent_out), _ptr(ws), ws.numel() * ws.element_size(),
+                                  _stream(stream)), "dit_denoise_step")
+
+
+def patchify(cfg: ModelConfig, vl: Varlen, latent, tokens, stream=None):
+    _check(lib().dit_patchify(ctypes.byref(cfg.c), ctypes.byref(vl.c), _ptr(latent), _ptr(tokens), _stream(stream)),
+           "dit_patchify")
+
+
+def unpatchify_euler(cfg: ModelConfig, vl: Varlen, latent, v, dt, latent_out, stream=None):
+    _check(lib().dit_unpatchify_euler(ctypes.byref(cfg.c), ctypes.byref(vl.c), _ptr(latent), _ptr(v), _ptr(dt),
+                                      _ptr(latent_out), _stream(stream)), "dit_unpatchify_euler")

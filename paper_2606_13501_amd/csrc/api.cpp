@@ -153,12 +153,17 @@ dit_status check_cfg(const dit_block_config* c) {
   return DIT_OK;
 }
 
-dit_status check_weights(const dit_block_config* c, const dit_block_weights* w, bool pre, bool post) {
+// tmlp: the block's own timestep MLP is read (not by the denoising step, whose
+// blocks share the model's).
+dit_status check_weights(const dit_block_config* c, const dit_block_weights* w, bool pre, bool post,
+                         bool tmlp = true) {
   if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
   const bool qn = c->qk_norm != 0;
-  if (pre) {
+  if (pre && tmlp) {
     DIT_TRY(check_ptr(w->w_t1, "w_t1")); DIT_TRY(check_ptr(w->b_t1, "b_t1"));
     DIT_TRY(check_ptr(w->w_t2, "w_t2")); DIT_TRY(check_ptr(w->b_t2, "b_t2"));
+  }
+  if (pre) {
     DIT_TRY(check_ptr(w->w_ada, "w_ada")); DIT_TRY(check_ptr(w->b_ada, "b_ada"));
     DIT_TRY(check_ptr(w->w_qkv, "w_qkv")); DIT_TRY(check_ptr(w->b_qkv, "b_qkv"));
     DIT_TRY(check_ptr(w->g_q, "g_q", !qn)); DIT_TRY(check_ptr(w->g_k, "g_k", !qn));
@@ -277,7 +282,7 @@ dit_status run_cond(const dit_block_config* c, const dit_block_weights* w, int n
   CondArgs p;
   p.t = t; p.n_req = n_req; p.freq_dim = c->freq_dim; p.hidden = c->hidden;
   p.w_t1 = w->w_t1; p.b_t1 = w->b_t1; p.w_t2 = w->w_t2; p.b_t2 = w->b_t2; p.w_ada = w->w_ada; p.b_ada = w->b_ada;
-  p.e = e; p.a1 = a1; p.c = cc; p.mod = mod; p.dtype = c->dtype;
+  p.n_mod = 6; p.e = e; p.a1 = a1; p.c = cc; p.mod = mod; p.dtype = c->dtype;
   return hip_status(launch_conditioning(p, s), "timestep conditioning");
 }
 
@@ -300,10 +305,26 @@ dit_status pre_attention_impl(const dit_block_config* c, const dit_block_weights
   return DIT_OK;
 }
 
+// Cross-attention keys and values of one block: kv = [RMS(txt W_ck^T + b_ck) | txt W_cv^T + b_cv].
+dit_status text_kv_impl(const dit_block_config* c, const dit_block_weights* w, int64_t L, const ReqTable& req_txt,
+                        const void* txt, void* kv, hipStream_t s) {
+  const int D = c->hidden;
+  DIT_TRY(run_linear(txt, D, w->w_ckv, D, w->b_ckv, kv, 2 * D, L, 2 * D, D, DIT_EPI_NONE, nullptr, 0, nullptr, 0,
+                     req_txt, c->dtype, s, "text key/value projection"));
+  if (c->qk_norm) {
+    const int zero[3] = {0, 0, 0};
+    DIT_TRY(run_norm_rope(kv, nullptr, 2 * D, L, c->n_heads, c->head_dim, w->g_ck, nullptr, c->rms_eps, zero, 0.f,
+                          nullptr, c->dtype, s));
+  }
+  return DIT_OK;
+}
+
 // S5..S12 on this GPU's rows given the self-attention output o.
+// With kv != NULL the text keys and values come from that cache ([txt_rows, 2D],
+// normalised keys) and txt is not read.
 dit_status post_attention_impl(const dit_block_config* c, const dit_block_weights* w, const dit_varlen* vl,
                                const void* x, const void* o, const void* txt, const float* mod, void* y,
-                               const Workspace& ws, hipStream_t s) {
+                               const Workspace& ws, hipStream_t s, const void* kv = nullptr) {
   const int D = c->hidden, Dff = c->mlp_hidden;
   const int64_t T = vl->cu_seqlens[vl->n_req];
   const int64_t L = vl->cu_seqlens_txt[vl->n_req];
@@ -318,18 +339,19 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   DIT_TRY(run_ln_affine(ws.x1, w->g_ca, w->b_ca, T, D, c->ln_eps, ws.h, dt, s));
   DIT_TRY(run_linear(ws.h, D, w->w_cq, D, w->b_cq, ws.cq, D, T, D, D, DIT_EPI_NONE, nullptr, 0, nullptr, 0, req, dt,
                      s, "cross query projection"));
-  // [ck | cv] = txt W_ckv^T + b_ckv ; ck = RMS(ck)
-  DIT_TRY(run_linear(txt, D, w->w_ckv, D, w->b_ckv, ws.ckv, 2 * D, L, 2 * D, D, DIT_EPI_NONE, nullptr, 0, nullptr,
-                     0, req_txt, dt, s, "text key/value projection"));
   if (c->qk_norm) {
     const int zero[3] = {0, 0, 0};
     DIT_TRY(run_norm_rope(ws.cq, nullptr, D, T, c->n_heads, c->head_dim, w->g_cq, nullptr, c->rms_eps, zero, 0.f,
                           nullptr, dt, s));
-    DIT_TRY(run_norm_rope(ws.ckv, nullptr, 2 * D, L, c->n_heads, c->head_dim, w->g_ck, nullptr, c->rms_eps, zero,
-                          0.f, nullptr, dt, s));
+  }
+  // [ck | cv] = txt W_ckv^T + b_ckv ; ck = RMS(ck)
+  const char* ckv = (const char*)kv;
+  if (!ckv) {
+    DIT_TRY(text_kv_impl(c, w, L, req_txt, txt, ws.ckv, s));
+    ckv = ws.ckv;
   }
   // oc = cross attention (queries: the request's latent rows, keys: its text rows)
-  DIT_TRY(run_attention(ws.cq, ws.ckv, ws.ckv + D * es, ws.o, D, 2 * D, 2 * D, D, req, req_txt, c->n_heads,
+  DIT_TRY(run_attention(ws.cq, ckv, ckv + D * es, ws.o, D, 2 * D, 2 * D, D, req, req_txt, c->n_heads,
                         c->head_dim, 1.0f / sqrtf((float)c->head_dim), dt, s));
   // x2 = x1 + (oc W_co^T + b_co), in place in x1
   DIT_TRY(run_linear(ws.o, D, w->w_co, D, w->b_co, ws.x1, D, T, D, D, DIT_EPI_RESIDUAL, ws.x1, D, nullptr, 0, req,
@@ -353,6 +375,112 @@ dit_status check_block_call(const dit_block_config* c, const dit_block_weights* 
     DIT_TRY(check_rope_table(vl, c->rope_sections, &tab));
   }
   return DIT_OK;
+}
+
+
+// ------------------------------------------------------------ denoising step
+
+int patch_len(const dit_model_config* m) { return m->in_channels * m->patch[0] * m->patch[1] * m->patch[2]; }
+
+dit_status check_model_cfg(const dit_model_config* m) {
+  if (!m) return fail(DIT_ERR_INVALID_ARG, "model config is NULL");
+  DIT_TRY(check_cfg(&m->block));
+  if (m->n_blocks < 1) return fail(DIT_ERR_INVALID_ARG, "n_blocks = %d", m->n_blocks);
+  if (m->in_channels < 1 || m->patch[0] < 1 || m->patch[1] < 1 || m->patch[2] < 1)
+    return fail(DIT_ERR_INVALID_ARG, "in_channels %d, patch (%d,%d,%d) must be >= 1", m->in_channels, m->patch[0],
+                m->patch[1], m->patch[2]);
+  const int64_t P = (int64_t)m->in_channels * m->patch[0] * m->patch[1] * m->patch[2];
+  if (P > (1 << 16)) return fail(DIT_ERR_UNSUPPORTED, "patch vector of %lld values", (long long)P);
+  if (m->block.dtype == DIT_BF16 && P % 64)
+    return fail(DIT_ERR_UNSUPPORTED, "bf16 needs C*pt*ph*pw %% 64 == 0 (it is %lld)", (long long)P);
+  if (m->block.dtype == DIT_F32 && P % 4)
+    return fail(DIT_ERR_UNSUPPORTED, "fp32 needs C*pt*ph*pw %% 4 == 0 (it is %lld)", (long long)P);
+  return DIT_OK;
+}
+
+// Whole requests only; fills the latent geometry.
+dit_status check_model_varlen(const dit_model_config* m, const dit_varlen* vl, LatentTable* tab) {
+  DIT_TRY(check_varlen(vl, true));
+  if (!vl->grid_fhw) return fail(DIT_ERR_INVALID_ARG, "grid_fhw is NULL");
+  memset(tab, 0, sizeof(*tab));
+  tab->n_req = vl->n_req;
+  tab->C = m->in_channels;
+  tab->pt = m->patch[0]; tab->ph = m->patch[1]; tab->pw = m->patch[2];
+  const int64_t P = patch_len(m);
+  for (int r = 0; r < vl->n_req; ++r) {
+    const int F = vl->grid_fhw[3 * r], H = vl->grid_fhw[3 * r + 1], W = vl->grid_fhw[3 * r + 2];
+    if (F < 1 || H < 1 || W < 1) return fail(DIT_ERR_INVALID_ARG, "grid of request %d is (%d,%d,%d)", r, F, H, W);
+    const int64_t cells = (int64_t)F * H * W;
+    const int rows = vl->cu_seqlens[r + 1] - vl->cu_seqlens[r];
+    if (cells != rows)
+      return fail(DIT_ERR_INVALID_ARG, "request %d has %d rows, its whole grid has %lld tokens", r, rows,
+                  (long long)cells);
+    if (vl->pos_offset && vl->pos_offset[r] != 0)
+      return fail(DIT_ERR_INVALID_ARG, "request %d: pos_offset %d (the step needs whole requests)", r,
+                  vl->pos_offset[r]);
+    tab->lat_off[r + 1] = tab->lat_off[r] + cells * P;
+    tab->row0[r] = vl->cu_seqlens[r];
+    tab->grid_h[r] = H;
+    tab->grid_w[r] = W;
+  }
+  return DIT_OK;
+}
+
+dit_status check_model_weights(const dit_model_config* m, const dit_model_weights* w) {
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "model weights is NULL");
+  DIT_TRY(check_ptr(w->w_t1, "w_t1")); DIT_TRY(check_ptr(w->b_t1, "b_t1"));
+  DIT_TRY(check_ptr(w->w_t2, "w_t2")); DIT_TRY(check_ptr(w->b_t2, "b_t2"));
+  DIT_TRY(check_ptr(w->w_pe, "w_pe")); DIT_TRY(check_ptr(w->b_pe, "b_pe"));
+  DIT_TRY(check_ptr(w->w_hmod, "w_hmod")); DIT_TRY(check_ptr(w->b_hmod, "b_hmod"));
+  DIT_TRY(check_ptr(w->w_out, "w_out")); DIT_TRY(check_ptr(w->b_out, "b_out"));
+  if (!w->blocks) return fail(DIT_ERR_INVALID_ARG, "blocks is NULL");
+  for (int b = 0; b < m->n_blocks; ++b) {
+    const dit_status st = check_weights(&m->block, &w->blocks[b], true, true, false);
+    if (st != DIT_OK) return fail(st, "block %d: %s", b, g_last_error.c_str());
+  }
+  return DIT_OK;
+}
+
+struct ModelWorkspace {
+  char *x, *tok;
+  Workspace blk;
+};
+
+// x [rows, D] (the residual stream), tok [rows, P] (patch vectors, then the
+// velocity), then a block workspace without text keys/values (they are cached).
+size_t model_layout(const dit_model_config* m, const dit_varlen* vl, char* base, ModelWorkspace* ws) {
+  const size_t es = elem_size(m->block.dtype);
+  const size_t T = vl->cu_seqlens[vl->n_req];
+  size_t off = 0;
+  ModelWorkspace w;
+  w.x = base ? base + off : nullptr;
+  off += round256(T * m->block.hidden * es);
+  w.tok = base ? base + off : nullptr;
+  off += round256(T * patch_len(m) * es);
+  dit_varlen no_txt = *vl;
+  no_txt.cu_seqlens_txt = nullptr;
+  off += layout(&m->block, &no_txt, base ? base + off : nullptr, &w.blk);
+  if (ws) *ws = w;
+  return off;
+}
+
+dit_status run_latent(bool euler, const dit_model_config* m, const LatentTable& tab, const float* latent,
+                      void* tokens, const float* dt, float* out, hipStream_t s) {
+  LatentArgs p;
+  p.latent = latent; p.tokens = tokens; p.dt = dt; p.latent_out = out; p.tab = tab; p.dtype = m->block.dtype;
+  return euler ? hip_status(launch_unpatchify_euler(p, s), "unpatchify + Euler update")
+               : hip_status(launch_patchify(p, s), "patchify");
+}
+
+// The conditioning chain with explicit parts (see CondArgs).
+dit_status run_cond_parts(const dit_block_config* c, int n_req, const float* t, const void* w_t1, const void* b_t1,
+                          const void* w_t2, const void* b_t2, const void* w_mod, const void* b_mod, int n_mod,
+                          float* mod, const Workspace& ws, hipStream_t s, const char* what) {
+  CondArgs p;
+  p.t = t; p.n_req = n_req; p.freq_dim = c->freq_dim; p.hidden = c->hidden;
+  p.w_t1 = w_t1; p.b_t1 = b_t1; p.w_t2 = w_t2; p.b_t2 = b_t2; p.w_ada = w_mod; p.b_ada = b_mod; p.n_mod = n_mod;
+  p.e = ws.e; p.a1 = ws.a1; p.c = ws.c; p.mod = mod; p.dtype = c->dtype;
+  return hip_status(launch_conditioning(p, s), what);
 }
 
 }  // namespace
@@ -586,6 +714,115 @@ dit_status dit_gated_residual(const void* x, const void* z, const void* bias, co
   p.x = x; p.z = z; p.bias = bias; p.gate = gate; p.gate_stride = gate_stride; p.out = out;
   p.n_rows = cu_seqlens[n_req]; p.hidden = hidden; p.req = make_req(cu_seqlens, n_req); p.dtype = dtype;
   return hip_status(launch_gated_residual(p, stream), "gated_residual");
+}
+
+size_t dit_text_kv_elems(const dit_model_config* cfg, const dit_varlen* vl) {
+  if (check_model_cfg(cfg) != DIT_OK || check_varlen(vl, true) != DIT_OK) return 0;
+  return (size_t)cfg->n_blocks * vl->cu_seqlens_txt[vl->n_req] * 2 * cfg->block.hidden;
+}
+
+dit_status dit_text_kv(const dit_model_config* cfg, const dit_model_weights* w, const dit_varlen* vl,
+                       const void* txt, void* kv, hipStream_t stream) {
+  g_last_error.clear();
+  DIT_TRY(check_model_cfg(cfg));
+  DIT_TRY(check_varlen(vl, true));
+  if (!w || !w->blocks) return fail(DIT_ERR_INVALID_ARG, "model weights or their blocks are NULL");
+  const dit_block_config* c = &cfg->block;
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    const dit_block_weights* bw = &w->blocks[b];
+    if (check_ptr(bw->w_ckv, "w_ckv") != DIT_OK || check_ptr(bw->b_ckv, "b_ckv") != DIT_OK ||
+        check_ptr(bw->g_ck, "g_ck", !c->qk_norm) != DIT_OK)
+      return fail(DIT_ERR_INVALID_ARG, "block %d: %s", b, g_last_error.c_str());
+  }
+  DIT_TRY(check_ptr(txt, "txt"));
+  DIT_TRY(check_ptr(kv, "kv"));
+  const int64_t L = vl->cu_seqlens_txt[vl->n_req];
+  const ReqTable req_txt = make_req(vl->cu_seqlens_txt, vl->n_req);
+  const size_t per_block = (size_t)L * 2 * c->hidden * elem_size(c->dtype);
+  for (int b = 0; b < cfg->n_blocks; ++b)
+    DIT_TRY(text_kv_impl(c, &w->blocks[b], L, req_txt, txt, (char*)kv + b * per_block, stream));
+  return DIT_OK;
+}
+
+size_t dit_denoise_workspace_size(const dit_model_config* cfg, const dit_varlen* vl) {
+  LatentTable tab;
+  if (check_model_cfg(cfg) != DIT_OK || check_model_varlen(cfg, vl, &tab) != DIT_OK) return 0;
+  return model_layout(cfg, vl, nullptr, nullptr);
+}
+
+dit_status dit_denoise_step(const dit_model_config* cfg, const dit_model_weights* w, const dit_varlen* vl,
+                            const float* latent, const float* t, const float* dt, const void* kv, float* latent_out,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_last_error.clear();
+  DIT_TRY(check_model_cfg(cfg));
+  LatentTable tab;
+  DIT_TRY(check_model_varlen(cfg, vl, &tab));
+  DIT_TRY(check_model_weights(cfg, w));
+  const dit_block_config* c = &cfg->block;
+  RopeTable rope;
+  DIT_TRY(check_rope_table(vl, c->rope_sections, &rope));
+  DIT_TRY(check_ptr(latent, "latent")); DIT_TRY(check_ptr(t, "t")); DIT_TRY(check_ptr(dt, "dt"));
+  DIT_TRY(check_ptr(kv, "kv")); DIT_TRY(check_ptr(latent_out, "latent_out"));
+  const size_t need = model_layout(cfg, vl, nullptr, nullptr);
+  if (!ws) return fail(DIT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)ws & 255u) != 0) return fail(DIT_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (ws_bytes < need) return fail(DIT_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  ModelWorkspace W;
+  model_layout(cfg, vl, (char*)ws, &W);
+
+  const int D = c->hidden, P = patch_len(cfg), R = vl->n_req;
+  const int64_t T = vl->cu_seqlens[R], L = vl->cu_seqlens_txt[R];
+  const size_t es = elem_size(c->dtype);
+  const dit_dtype dty = c->dtype;
+  const ReqTable req = make_req(vl->cu_seqlens, R);
+  const float scale = 1.0f / sqrtf((float)c->head_dim);
+  // x = patchify(latent) W_pe^T + b_pe
+  DIT_TRY(run_latent(false, cfg, tab, latent, W.tok, nullptr, nullptr, stream));
+  DIT_TRY(run_linear(W.tok, P, w->w_pe, P, w->b_pe, W.x, D, T, D, P, DIT_EPI_NONE, nullptr, 0, nullptr, 0, req, dty,
+                     stream, "patch embedding"));
+  // SiLU(c) of the shared timestep MLP, once for all blocks
+  DIT_TRY(run_cond_parts(c, R, t, w->w_t1, w->b_t1, w->w_t2, w->b_t2, nullptr, nullptr, 0, nullptr, W.blk, stream,
+                         "timestep MLP"));
+  const Workspace& B = W.blk;
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    const dit_block_weights* bw = &w->blocks[b];
+    DIT_TRY(run_cond_parts(c, R, t, nullptr, nullptr, nullptr, nullptr, bw->w_ada, bw->b_ada, 6, B.mod, B, stream,
+                           "block modulation"));
+    DIT_TRY(pre_attention_impl(c, bw, vl, W.x, B.mod, B.qkv, B, stream));
+    DIT_TRY(run_attention(B.qkv, B.qkv + D * es, B.qkv + 2 * D * es, B.o, 3 * D, 3 * D, 3 * D, D, req, req,
+                          c->n_heads, c->head_dim, scale, dty, stream));
+    DIT_TRY(post_attention_impl(c, bw, vl, W.x, B.o, nullptr, B.mod, W.x, B, stream,
+                                (const char*)kv + (size_t)b * L * 2 * D * es));
+  }
+  // output layer: v = (LN(x)(1 + scale) + shift) W_out^T + b_out with (shift, scale) = W_hmod SiLU(c) + b_hmod
+  DIT_TRY(run_cond_parts(c, R, t, nullptr, nullptr, nullptr, nullptr, w->w_hmod, w->b_hmod, 2, B.mod, B, stream,
+                         "output modulation"));
+  DIT_TRY(run_ln_mod(W.x, B.mod, B.mod + D, 2 * D, req, T, D, c->ln_eps, B.h, dty, stream));
+  DIT_TRY(run_linear(B.h, D, w->w_out, D, w->b_out, W.tok, P, T, P, D, DIT_EPI_NONE, nullptr, 0, nullptr, 0, req, dty,
+                     stream, "output projection"));
+  // latent_out = latent + dt * unpatchify(v)
+  return run_latent(true, cfg, tab, latent, W.tok, dt, latent_out, stream);
+}
+
+dit_status dit_patchify(const dit_model_config* cfg, const dit_varlen* vl, const float* latent, void* tokens,
+                        hipStream_t stream) {
+  g_last_error.clear();
+  DIT_TRY(check_model_cfg(cfg));
+  LatentTable tab;
+  DIT_TRY(check_model_varlen(cfg, vl, &tab));
+  DIT_TRY(check_ptr(latent, "latent")); DIT_TRY(check_ptr(tokens, "tokens"));
+  return run_latent(false, cfg, tab, latent, tokens, nullptr, nullptr, stream);
+}
+
+dit_status dit_unpatchify_euler(const dit_model_config* cfg, const dit_varlen* vl, const float* latent, const void* v,
+                                const float* dt, float* latent_out, hipStream_t stream) {
+  g_last_error.clear();
+  DIT_TRY(check_model_cfg(cfg));
+  LatentTable tab;
+  DIT_TRY(check_model_varlen(cfg, vl, &tab));
+  DIT_TRY(check_ptr(latent, "latent")); DIT_TRY(check_ptr(v, "v")); DIT_TRY(check_ptr(dt, "dt"));
+  DIT_TRY(check_ptr(latent_out, "latent_out"));
+  return run_latent(true, cfg, tab, latent, const_cast<void*>(v), dt, latent_out, stream);
 }
 
 }  // extern "C"

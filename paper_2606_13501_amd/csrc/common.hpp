@@ -34,6 +34,18 @@ struct RopeTable {
   int offset[DIT_MAX_REQ];    // flattened grid index of the first row
 };
 
+// Geometry of the packed latent of a denoising step: request r's fp32 latent
+// [C, F*pt, H*ph, W*pw] occupies elements lat_off[r]..lat_off[r+1]; its tokens
+// are rows row0[r].. of the token matrix in (f, h, w) order.
+struct LatentTable {
+  int n_req;
+  int C, pt, ph, pw;
+  int64_t lat_off[DIT_MAX_REQ + 1];
+  int row0[DIT_MAX_REQ];
+  int grid_h[DIT_MAX_REQ];
+  int grid_w[DIT_MAX_REQ];
+};
+
 __device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
 __device__ __forceinline__ bf16 f2bf(float v) { return (bf16)v; }
 

@@ -76,13 +76,29 @@ struct GatedResArgs {
 hipError_t launch_gated_residual(const GatedResArgs& p, hipStream_t s);
 
 // Timestep conditioning: e (fp32 [R,F]) -> ... -> mod (fp32 [R,6D]).
+// Timestep conditioning in two optional parts:
+//  - w_t1 != NULL: e = sinusoid(t), a1 = SiLU(W_t1 e + b_t1), c = SiLU(W_t2 a1 + b_t2)
+//    (c holds SiLU of the timestep MLP's output, the input of every modulation);
+//  - w_ada != NULL: mod = W_ada c + b_ada with n_mod*hidden outputs per request.
 struct CondArgs {
   const float* t; int n_req; int freq_dim; int hidden;
   const void *w_t1, *b_t1, *w_t2, *b_t2, *w_ada, *b_ada;
+  int n_mod;
   float* e; float* a1; float* c;   // scratch [R,F], [R,D], [R,D]
   float* mod;
   dit_dtype dtype;
 };
 hipError_t launch_conditioning(const CondArgs& p, hipStream_t s);
+
+struct LatentArgs {
+  const float* latent;   // fp32 packed latent
+  void* tokens;          // [rows, P] dtype (patchify: written; Euler: the velocity, read)
+  const float* dt;       // device [n_req] (Euler only)
+  float* latent_out;     // Euler only; may equal latent
+  LatentTable tab;
+  dit_dtype dtype;
+};
+hipError_t launch_patchify(const LatentArgs& p, hipStream_t s);
+hipError_t launch_unpatchify_euler(const LatentArgs& p, hipStream_t s);
 
 }  // namespace dit

@@ -1,7 +1,7 @@
 // Memory-bound kernels of the DiT block: LayerNorm with adaLN modulation or a
 // shared affine, per-head RMSNorm with sectioned rotary embedding on q and k,
 // the standalone gated residual, and the timestep-conditioning chain
-// (sinusoid -> Linear-SiLU -> Linear-SiLU -> Linear to six modulation vectors).
+// (sinusoid -> Linear-SiLU -> Linear-SiLU -> Linear to the modulation vectors).
 //
 // Every kernel moves 16-byte vectors per lane with consecutive lanes on
 // consecutive addresses; a row is held in registers between its statistics
@@ -356,14 +356,19 @@ hipError_t ln_typed(const LnArgs& p, hipStream_t s) {
 
 template <typename T>
 hipError_t cond_typed(const CondArgs& p, hipStream_t s) {
-  const int half = p.freq_dim / 2;
-  timestep_embed_kernel<<<(p.n_req * half + 255) / 256, 256, 0, s>>>(p.t, p.e, p.n_req, p.freq_dim);
-  gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t1, (const T*)p.b_t1, p.e, p.a1,
-                                                         p.hidden, p.freq_dim, p.n_req);
-  gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t2, (const T*)p.b_t2, p.a1, p.c,
-                                                         p.hidden, p.hidden, p.n_req);
-  gemv_kernel<T, false><<<(6 * p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_ada, (const T*)p.b_ada, p.c,
-                                                              p.mod, 6 * p.hidden, p.hidden, p.n_req);
+  if (p.w_t1) {
+    const int half = p.freq_dim / 2;
+    timestep_embed_kernel<<<(p.n_req * half + 255) / 256, 256, 0, s>>>(p.t, p.e, p.n_req, p.freq_dim);
+    gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t1, (const T*)p.b_t1, p.e, p.a1,
+                                                           p.hidden, p.freq_dim, p.n_req);
+    gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t2, (const T*)p.b_t2, p.a1, p.c,
+                                                           p.hidden, p.hidden, p.n_req);
+  }
+  if (p.w_ada) {
+    const int n_out = p.n_mod * p.hidden;
+    gemv_kernel<T, false><<<(n_out + 3) / 4, 256, 0, s>>>((const T*)p.w_ada, (const T*)p.b_ada, p.c, p.mod,
+                                                         n_out, p.hidden, p.n_req);
+  }
   return hipGetLastError();
 }
 

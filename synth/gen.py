@@ -23,7 +23,7 @@ import os
 
 import numpy as np
 
-from .workloads import Workload
+from .workloads import ModelWorkload, Workload
 
 SEED = 13501
 CHUNK = 1 << 22
@@ -215,3 +215,52 @@ def draw(shape, key: Sequence[int], dtype: str = "bf16", dist: str = "normal", m
         for ch in chunks:
             work(ch)
     return out.reshape(spec.shape)
+
+
+MODEL_WEIGHT_NAMES = ("w_t1", "b_t1", "w_t2", "b_t2", "w_pe", "b_pe", "w_hmod", "b_hmod", "w_out", "b_out")
+
+
+def model_tensor_specs(mw: ModelWorkload) -> Dict[str, TensorSpec]:
+    """The step's own inputs and weights: the packed fp32 latent ~ N(0, 1),
+    t ~ U[0, 1000), dt ~ U[-0.05, -0.01) (one step of a 20..100-step schedule
+    towards sigma = 0), and the model-level weights."""
+    wl = mw.block
+    D, F, P = wl.hidden, wl.freq_dim, mw.patch_len
+    W = wl.linear_std
+    specs = [
+        TensorSpec("latent", 50, (sum(mw.latent_sizes()),), "normal", dtype="f32"),
+        TensorSpec("t", 51, (wl.n_req,), "uniform", lo=0.0, hi=1000.0, dtype="f32"),
+        TensorSpec("dt", 52, (wl.n_req,), "uniform", lo=-0.05, hi=-0.01, dtype="f32"),
+        TensorSpec("txt", 2, (wl.n_txt, D), "normal"),
+        TensorSpec("w_t1", 53, (D, F), "normal", std=W),
+        TensorSpec("b_t1", 54, (D,), "normal", std=0.02),
+        TensorSpec("w_t2", 55, (D, D), "normal", std=W),
+        TensorSpec("b_t2", 56, (D,), "normal", std=0.02),
+        TensorSpec("w_pe", 57, (D, P), "normal", std=W),
+        TensorSpec("b_pe", 58, (D,), "normal", std=0.02),
+        TensorSpec("w_hmod", 59, (2 * D, D), "normal", std=W),
+        TensorSpec("b_hmod", 60, (2 * D,), "normal", std=0.02),
+        TensorSpec("w_out", 61, (P, D), "normal", std=W),
+        TensorSpec("b_out", 62, (P,), "normal", std=0.02),
+    ]
+    return {s.name: s for s in specs}
+
+
+def generate_model_inputs(mw: ModelWorkload, threads: Optional[int] = None):
+    """(model tensors, [block weight dicts]).  Block b's weights use the block
+    recipe with tensor ids offset by 1000 * (b + 1); they omit the blocks' own
+    timestep MLP, which the step does not read."""
+    specs = model_tensor_specs(mw)
+    model = {n: generate_tensor(s, mw.block, threads) for n, s in specs.items()}
+    bspecs = block_tensor_specs(mw.block)
+    blocks = []
+    for b in range(mw.n_blocks):
+        d = {}
+        for n in WEIGHT_NAMES:
+            if n in ("w_t1", "b_t1", "w_t2", "b_t2"):
+                continue
+            s = bspecs[n]
+            d[n] = generate_tensor(TensorSpec(s.name, s.tid + 1000 * (b + 1), s.shape, s.dist, s.mean, s.std,
+                                              s.lo, s.hi, s.dtype), mw.block, threads)
+        blocks.append(d)
+    return model, blocks

@@ -109,3 +109,57 @@ def get_workload(name: str) -> Workload:
         return WORKLOADS[name]
     except KeyError:
         raise KeyError(f"unknown workload {name!r}; known: {sorted(WORKLOADS)}") from None
+
+
+@dataclass(frozen=True)
+class ModelWorkload:
+    """One denoising step: a block workload (its requests must be whole) plus
+    the model's depth, latent channels and patch size."""
+    name: str
+    block: Workload
+    n_blocks: int
+    in_channels: int
+    patch: Tuple[int, int, int]
+    description: str = ""
+
+    @property
+    def patch_len(self) -> int:
+        return self.in_channels * self.patch[0] * self.patch[1] * self.patch[2]
+
+    def latent_sizes(self) -> List[int]:
+        pt, ph, pw = self.patch
+        return [self.in_channels * f * pt * h * ph * w * pw for (f, h, w) in self.block.grids]
+
+
+def _whole(name, wid, dtype, D, H, d, Dff, F, sec, grids, L, desc, **kw):
+    rows = [f * h * w for (f, h, w) in grids]
+    return _w(name, wid, dtype, D, H, d, Dff, F, sec, grids, rows, L, desc, **kw)
+
+
+MODEL_WORKLOADS: Dict[str, ModelWorkload] = {}
+for _mw in [
+    ModelWorkload("step_tiny_fp32",
+                  _whole("step_tiny_fp32.block", 11, "f32", 384, 6, 64, 1536, 384, (16, 24, 24),
+                         [(2, 4, 6), (1, 8, 8)], 77, "two whole requests: 2x8x12 and 1x16x16 latents"),
+                  2, 4, (1, 2, 2),
+                  "tiny fp32 step: 2 blocks, 4 latent channels, patch 1x2x2, requests of 48 and 64 tokens"),
+    ModelWorkload("step_small_bf16",
+                  _whole("step_small_bf16.block", 12, "bf16", 256, 2, 128, 1024, 256, (44, 42, 42),
+                         [(3, 4, 6), (1, 6, 10)], 40, "two whole requests: 3x8x12 and 1x12x20 latents; weight "
+                         "matrices at std 0.02*sqrt(5120/256) so activations have the D = 5120 magnitudes",
+                         linear_std=0.02 * (5120 / 256) ** 0.5),
+                  2, 16, (1, 2, 2),
+                  "small bf16 step: 2 blocks, D 256, 16 latent channels, patch 1x2x2, requests of 72 and 60 tokens"),
+    ModelWorkload("step_video_480p", WORKLOADS["video_480p"], 40, 16, (1, 2, 2),
+                  "480p video step: 40 blocks of the 480p block, latent 16x21x60x104, patch 1x2x2"),
+    ModelWorkload("step_video_720p", WORKLOADS["video_720p"], 40, 16, (1, 2, 2),
+                  "720p video step: 40 blocks of the 720p block, latent 16x21x90x160, patch 1x2x2"),
+]:
+    MODEL_WORKLOADS[_mw.name] = _mw
+
+
+def get_model_workload(name: str) -> ModelWorkload:
+    try:
+        return MODEL_WORKLOADS[name]
+    except KeyError:
+        raise KeyError(f"unknown step workload {name!r}; known: {sorted(MODEL_WORKLOADS)}") from None

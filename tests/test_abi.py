@@ -159,3 +159,93 @@ def test_block_validation_and_workspace():
     vl = B.Varlen([0, 17, 40], [0, 8, 20], [(1, 4, 4), (1, 4, 6)])
     r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P, P, 1 << 40, S)
     assert r == B.DIT_ERR_INVALID_ARG and b"exceed its grid" in L.dit_last_error()
+
+
+# ---------------------------------------------------------------- the denoising step
+
+
+def _step_args(grids=((3, 4, 6), (1, 6, 10)), rows=None, C=16, patch=(1, 2, 2), n_blocks=2, dtype=None,
+               pos_offset=None):
+    dtype = B.DIT_BF16 if dtype is None else dtype
+    bc = B.BlockConfig(256, 2, 128, 1024, 256, (44, 42, 42), dtype)
+    cfg = B.ModelConfig(bc, n_blocks, C, patch)
+    rows = rows or [f * h * w for f, h, w in grids]
+    cu = np.cumsum([0] + list(rows))
+    vl = B.Varlen(cu, [40 * i for i in range(len(rows) + 1)], list(grids), pos_offset)
+    blk = B.CWeights()
+    for n in B.WEIGHT_FIELDS:
+        setattr(blk, n, P.value)
+    w = B.ModelWeights({}, [blk] * max(n_blocks, 1))
+    for n in B.MODEL_FIELDS:
+        setattr(w.c, n, P.value)
+    return cfg, vl, w
+
+
+def _step_call(cfg, vl, w, ws=None, ws_bytes=0, latent=P, kv=P):
+    L = _lib()
+    return L.dit_denoise_step(ctypes.byref(cfg.c), ctypes.byref(w.c), ctypes.byref(vl.c), latent, P, P, kv, P, ws,
+                              ws_bytes, ctypes.c_void_p(0))
+
+
+def test_denoise_step_sizes():
+    L = _lib()
+    cfg, vl, w = _step_args()
+    assert L.dit_text_kv_elems(ctypes.byref(cfg.c), ctypes.byref(vl.c)) == 2 * 80 * 2 * 256
+    need = L.dit_denoise_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c))
+    blk = L.dit_block_workspace_size(ctypes.byref(cfg.block.c), ctypes.byref(vl.c))
+    assert need > 0 and blk > 0
+    # x and the patch tokens on top of a block workspace without text keys/values
+    assert need >= 132 * 256 * 2 + 132 * 64 * 2
+    cfg2, vl2, _ = _step_args(rows=[72, 59])
+    assert L.dit_denoise_workspace_size(ctypes.byref(cfg2.c), ctypes.byref(vl2.c)) == 0
+
+
+def test_denoise_step_rejects_bad_arguments():
+    L = _lib()
+    cfg, vl, w = _step_args()
+    # valid arguments up to the workspace: fails on the workspace, launches nothing
+    assert _step_call(cfg, vl, w) == B.DIT_ERR_WORKSPACE
+    assert _step_call(cfg, vl, w, ws=P, ws_bytes=1024) == B.DIT_ERR_WORKSPACE
+    assert _step_call(cfg, vl, w, latent=None) == B.DIT_ERR_INVALID_ARG
+    assert _step_call(cfg, vl, w, kv=P_MIS) == B.DIT_ERR_INVALID_ARG
+    cfg2, vl2, w2 = _step_args(rows=[72, 59])
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_INVALID_ARG
+    assert b"whole grid" in L.dit_last_error()
+    cfg2, vl2, w2 = _step_args(pos_offset=[0, 4])
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_INVALID_ARG
+    assert b"pos_offset" in L.dit_last_error()
+    cfg2, vl2, w2 = _step_args(C=3)
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_UNSUPPORTED
+    cfg2, vl2, w2 = _step_args(C=3, patch=(1, 1, 1), grids=((3, 8, 12), (1, 12, 20)), dtype=B.DIT_F32)
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_UNSUPPORTED
+    cfg2, vl2, w2 = _step_args(patch=(1, 0, 2))
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_INVALID_ARG
+    cfg2, vl2, w2 = _step_args(n_blocks=0)
+    assert _step_call(cfg2, vl2, w2) == B.DIT_ERR_INVALID_ARG
+    w.c.w_out = None
+    assert _step_call(cfg, vl, w) == B.DIT_ERR_INVALID_ARG
+    assert b"w_out" in L.dit_last_error()
+    cfg, vl, w = _step_args()
+    w.blocks[1].w_qkv = None
+    assert _step_call(cfg, vl, w) == B.DIT_ERR_INVALID_ARG
+    assert b"block 1" in L.dit_last_error() and b"w_qkv" in L.dit_last_error()
+    cfg, vl, w = _step_args()
+    w.blocks[0].w_t1 = None     # the blocks' own timestep MLP is not read by the step
+    assert _step_call(cfg, vl, w) == B.DIT_ERR_WORKSPACE
+
+
+def test_text_kv_and_latent_stages_reject_bad_arguments():
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cfg, vl, w = _step_args()
+    assert L.dit_text_kv(ctypes.byref(cfg.c), ctypes.byref(w.c), ctypes.byref(vl.c), None, P, S) == \
+        B.DIT_ERR_INVALID_ARG
+    w.blocks[1].w_ckv = None
+    assert L.dit_text_kv(ctypes.byref(cfg.c), ctypes.byref(w.c), ctypes.byref(vl.c), P, P, S) == \
+        B.DIT_ERR_INVALID_ARG
+    assert b"block 1" in L.dit_last_error()
+    cfg2, vl2, _ = _step_args(rows=[72, 61])
+    assert L.dit_patchify(ctypes.byref(cfg2.c), ctypes.byref(vl2.c), P, P, S) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_unpatchify_euler(ctypes.byref(cfg.c), ctypes.byref(vl.c), P, P, None, P, S) == \
+        B.DIT_ERR_INVALID_ARG
+    assert L.dit_patchify(ctypes.byref(cfg.c), ctypes.byref(vl.c), P_MIS, P, S) == B.DIT_ERR_INVALID_ARG
