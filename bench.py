@@ -121,6 +121,137 @@ def cpu_baseline(wl, target_s=12.0):
                        f"float64 NumPy, {dt:.1f} s")}
 
 
+STEP_METRIC = "DiT denoising step ms + TFLOP/s (% bf16 MFMA peak): B blocks + patch embedding + output layer + Euler"
+
+
+def step_flops(mw):
+    """Algorithmic flops of one denoising step: B blocks without their own
+    timestep MLP and text key/value projection (shared and cached), plus the
+    shared timestep MLP, the patch embedding, the output modulation and
+    projection (the Euler update is 2 flops per latent value)."""
+    wl = mw.block
+    D, F, P, R = wl.hidden, wl.freq_dim, mw.patch_len, wl.n_req
+    fb = block_flops(wl)
+    per_block = fb["total"] - 2.0 * R * (D * F + D * D) - 2.0 * wl.n_txt * D * 2 * D
+    head = 2.0 * R * (D * F + D * D) + 2.0 * wl.n_rows * P * D * 2 + 2.0 * R * 2 * D * D
+    return {"blocks": mw.n_blocks * per_block, "self_attn": mw.n_blocks * fb["self_attn"],
+            "total": mw.n_blocks * per_block + head + 2.0 * sum(mw.latent_sizes())}
+
+
+def run_step(args):
+    """Time dit_denoise_step at a step workload (weights drawn on the device:
+    the block recipe's distributions from torch's seeded device generator, so
+    that 40 blocks of weights need no host round trip)."""
+    import torch
+    import synth
+    import paper_2606_13501_amd.binding as B
+    mw = synth.get_model_workload(args.step)
+    wl = mw.block
+    D, F, P, Dff, d = wl.hidden, wl.freq_dim, mw.patch_len, wl.mlp_hidden, wl.head_dim
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    g = torch.Generator(device="cuda")
+    g.manual_seed(13501)
+
+    def normal(shape, std=1.0, mean=0.0, dtype=tdt):
+        return (torch.randn(shape, generator=g, device="cuda") * std + mean).to(dtype)
+
+    t0 = time.time()
+    std = wl.linear_std
+    model = {"w_t1": normal((D, F), std), "b_t1": normal((D,), 0.02), "w_t2": normal((D, D), std),
+             "b_t2": normal((D,), 0.02), "w_pe": normal((D, P), std), "b_pe": normal((D,), 0.02),
+             "w_hmod": normal((2 * D, D), std), "b_hmod": normal((2 * D,), 0.02), "w_out": normal((P, D), std),
+             "b_out": normal((P,), 0.02)}
+    shapes = {"w_ada": (6 * D, D), "b_ada": (6 * D,), "w_qkv": (3 * D, D), "b_qkv": (3 * D,), "g_q": (d,),
+              "g_k": (d,), "w_o": (D, D), "b_o": (D,), "g_ca": (D,), "b_ca": (D,), "w_cq": (D, D), "b_cq": (D,),
+              "w_ckv": (2 * D, D), "b_ckv": (2 * D,), "g_cq": (d,), "g_ck": (d,), "w_co": (D, D), "b_co": (D,),
+              "w_up": (Dff, D), "b_up": (Dff,), "w_dn": (D, Dff), "b_dn": (D,)}
+    blocks = []
+    for _ in range(mw.n_blocks):
+        blk = {}
+        for n, shp in shapes.items():
+            if n.startswith("g_"):
+                blk[n] = normal(shp, 0.02, 1.0)
+            else:
+                blk[n] = normal(shp, std if len(shp) == 2 else 0.02)
+        blocks.append(blk)
+    latent = torch.randn((sum(mw.latent_sizes()),), generator=g, device="cuda")
+    txt = normal((wl.n_txt, D))
+    t = torch.rand((wl.n_req,), generator=g, device="cuda") * 1000.0
+    dt = -0.01 - 0.04 * torch.rand((wl.n_req,), generator=g, device="cuda")
+    torch.cuda.synchronize()
+    print(f"[bench] drew {mw.name} weights on the device in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    bc = B.BlockConfig(D, wl.n_heads, d, Dff, F, wl.rope_sections, tdt)
+    cfg = B.ModelConfig(bc, mw.n_blocks, mw.in_channels, mw.patch)
+    w = B.ModelWeights(model, [B.make_weights(b) for b in blocks])
+    vl = B.Varlen(wl.cu_seqlens(), wl.cu_txt(), list(wl.grids))
+    ws = torch.empty(B.denoise_workspace_size(cfg, vl), dtype=torch.uint8, device="cuda")
+    kv = torch.empty(B.text_kv_elems(cfg, vl), dtype=tdt, device="cuda")
+    stream = torch.cuda.current_stream()
+    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    k0.record(stream)
+    B.text_kv(cfg, w, vl, txt, kv)
+    k1.record(stream)
+    lat = [latent, torch.empty_like(latent)]
+
+    def one(i):
+        B.denoise_step(cfg, w, vl, lat[i % 2], t, dt, kv, lat[(i + 1) % 2], ws)
+
+    for i in range(args.warmup):
+        one(i)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup step {i} done", file=sys.stderr, flush=True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        one(args.warmup + i)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    if not torch.isfinite(lat[(args.warmup + args.steps) % 2]).all():
+        raise RuntimeError("non-finite latent after the timed steps")
+    fl = step_flops(mw)
+    tflops = fl["total"] / (ms * 1e-3) / 1e12
+    out = {
+        "metric": STEP_METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded device draws; random-init weights of the block recipe's distributions)",
+        "config": {
+            "workload": mw.name, "blocks": mw.n_blocks, "tokens": wl.n_rows, "requests": wl.n_req, "hidden": D,
+            "heads": wl.n_heads, "head_dim": d, "mlp_hidden": Dff, "text_tokens": wl.n_txt,
+            "latent_channels": mw.in_channels, "patch": list(mw.patch), "step_flops": fl["total"],
+            "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
+            "ms_text_kv_once_per_request": round(k0.elapsed_time(k1), 3),
+            "ms_per_block": round(ms / mw.n_blocks, 3),
+        },
+        "roofline": {
+            "kernel": "whole step (per-kernel durations: rocprofv3 kernel statistics of this command)",
+            "bound": "mfma",
+            "achieved": round(tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"]["sample"] += " (the oracle's rate on one block's work; a step is B such blocks)"
+        print(f"[bench] cpu baseline took {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    print(json.dumps(out), flush=True)
+
+
 def profile_kernel(args, wl):
     """One kernel alone, args.steps times, for counter collection."""
     import torch
@@ -157,6 +288,9 @@ def main():
                     help="run only one kernel (for rocprofv3 counter passes) and exit: the block's "
                          "self-attention at the workload's shape, or a plain 1 GiB device copy used to "
                          "calibrate the HBM byte counters")
+    ap.add_argument("--step", default=None, metavar="STEP_WORKLOAD",
+                    help="time one whole denoising step (dit_denoise_step) at this step workload, e.g. "
+                         "step_video_720p, instead of the block; prints its own JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -173,6 +307,9 @@ def main():
         sys.exit(1)
     B.lib()
     torch.cuda.set_device(0)
+    if args.step:
+        run_step(args)
+        return
     wl = synth.get_workload(args.workload)
     if args.profile_kernel:
         profile_kernel(args, wl)

@@ -390,7 +390,7 @@ dit_status check_model_cfg(const dit_model_config* m) {
     return fail(DIT_ERR_INVALID_ARG, "in_channels %d, patch (%d,%d,%d) must be >= 1", m->in_channels, m->patch[0],
                 m->patch[1], m->patch[2]);
   const int64_t P = (int64_t)m->in_channels * m->patch[0] * m->patch[1] * m->patch[2];
-  if (P > (1 << 16)) return fail(DIT_ERR_UNSUPPORTED, "patch vector of %lld values", (long long)P);
+  if (P > 8192) return fail(DIT_ERR_UNSUPPORTED, "patch vector of %lld values (at most 8192)", (long long)P);
   if (m->block.dtype == DIT_BF16 && P % 64)
     return fail(DIT_ERR_UNSUPPORTED, "bf16 needs C*pt*ph*pw %% 64 == 0 (it is %lld)", (long long)P);
   if (m->block.dtype == DIT_F32 && P % 4)
@@ -407,6 +407,11 @@ dit_status check_model_varlen(const dit_model_config* m, const dit_varlen* vl, L
   tab->C = m->in_channels;
   tab->pt = m->patch[0]; tab->ph = m->patch[1]; tab->pw = m->patch[2];
   const int64_t P = patch_len(m);
+  // tiles of about 2048 patch values (the latent kernels' LDS transpose)
+  int max_w = 1;
+  for (int r = 0; r < vl->n_req; ++r) max_w = vl->grid_fhw[3 * r + 2] > max_w ? vl->grid_fhw[3 * r + 2] : max_w;
+  tab->wt = (int)(2048 / P) < 1 ? 1 : (int)(2048 / P);
+  if (tab->wt > max_w) tab->wt = max_w;
   for (int r = 0; r < vl->n_req; ++r) {
     const int F = vl->grid_fhw[3 * r], H = vl->grid_fhw[3 * r + 1], W = vl->grid_fhw[3 * r + 2];
     if (F < 1 || H < 1 || W < 1) return fail(DIT_ERR_INVALID_ARG, "grid of request %d is (%d,%d,%d)", r, F, H, W);
@@ -419,6 +424,9 @@ dit_status check_model_varlen(const dit_model_config* m, const dit_varlen* vl, L
       return fail(DIT_ERR_INVALID_ARG, "request %d: pos_offset %d (the step needs whole requests)", r,
                   vl->pos_offset[r]);
     tab->lat_off[r + 1] = tab->lat_off[r] + cells * P;
+    const int64_t tiles = tab->tile_off[r] + (int64_t)F * H * ((W + tab->wt - 1) / tab->wt);
+    if (tiles > 0x7FFFFFFF) return fail(DIT_ERR_UNSUPPORTED, "latent of %lld tiles", (long long)tiles);
+    tab->tile_off[r + 1] = (int)tiles;
     tab->row0[r] = vl->cu_seqlens[r];
     tab->grid_h[r] = H;
     tab->grid_w[r] = W;

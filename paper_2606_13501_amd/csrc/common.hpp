@@ -13,6 +13,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -36,11 +37,15 @@ struct RopeTable {
 
 // Geometry of the packed latent of a denoising step: request r's fp32 latent
 // [C, F*pt, H*ph, W*pw] occupies elements lat_off[r]..lat_off[r+1]; its tokens
-// are rows row0[r].. of the token matrix in (f, h, w) order.
+// are rows row0[r].. of the token matrix in (f, h, w) order.  The latent
+// kernels work in tiles of up to `wt` consecutive tokens of one (f, h) token
+// row; request r owns tiles tile_off[r]..tile_off[r+1].
 struct LatentTable {
   int n_req;
   int C, pt, ph, pw;
+  int wt;
   int64_t lat_off[DIT_MAX_REQ + 1];
+  int tile_off[DIT_MAX_REQ + 1];
   int row0[DIT_MAX_REQ];
   int grid_h[DIT_MAX_REQ];
   int grid_w[DIT_MAX_REQ];
