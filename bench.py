@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "DiT block fwd ms + TFLOP/s (% bf16 MFMA peak) at 32K/75K video tokens"
 PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "attn_fwd_bf16.video_720p.traffic.txt")
 ATTN_SOURCE = os.path.join(ROOT, "paper_2606_13501_amd", "csrc", "attention.hip")
@@ -111,8 +112,8 @@ def cpu_baseline(wl, target_s=12.0):
             + 2.0 * wl.txt_len * D * 2 * D + 2.0 * (D * wl.freq_dim + 7 * D * D)
         return dt, fl
 
-    dt, fl = run(16)
-    n = int(min(4096, max(16, 16 * target_s / max(dt, 1e-3))))
+    dt, fl = run(min(16, n_all))
+    n = int(min(4096, n_all, max(16, 16 * target_s / max(dt, 1e-3))))
     dt, fl = run(n)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": (f"{wl.name}: all block steps for {n} evenly spaced query rows of the "
@@ -277,6 +278,100 @@ def profile_kernel(args, wl):
     print(json.dumps({"profile": "attention", "workload": wl.name, "launches": args.steps}), flush=True)
 
 
+def gpu_clocks():
+    """Current graphics clock, memory clock and power of GPU 0 from amd-smi, or
+    None where the tool is not available."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--power", "--json"], capture_output=True,
+                           text=True, timeout=30)
+        data = json.loads(r.stdout)
+    except Exception:
+        return None
+    out = {}
+
+    def walk(x, path):
+        if isinstance(x, dict):
+            if "value" in x and not isinstance(x["value"], (dict, list)):
+                out[path] = f"{x['value']} {x.get('unit', '')}".strip()
+                return
+            for k, v in x.items():
+                walk(v, f"{path}.{k}" if path else k)
+        elif isinstance(x, list):
+            for i, v in enumerate(x):
+                walk(v, path)
+
+    walk(data, "")
+    keep = {k: v for k, v in out.items()
+            if any(t in k for t in ("gfx_0.clk", "mem_0.clk", "socket_power", "current_socket_power"))}
+    return keep or None
+
+
+def oracle_seconds(wl):
+    """The float64 oracle on the workload's whole block, as it stands, on the
+    host cores, timed by stages: conditioning and pre-attention on the rows,
+    self-attention one (request, head) at a time with the oracle's attention
+    (the loop its varlen attention runs, here with a progress line per head),
+    post-attention on the rows.  For a sequence-parallel share the
+    self-attention runs over the full lengths with the share's heads on the
+    seeded q, k, v, and post-attention on the seeded attention output of the
+    share's rows.  Prints seconds and fp64 GFLOP/s of the block's algorithmic
+    work."""
+    import numpy as np
+    import synth
+    from oracle import dit_block as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = max([i.get("num_threads", 1) for i in blas] or [1])
+        vendor = ",".join(sorted({i.get("internal_api", "?") for i in blas}))
+    except Exception:
+        cores, vendor = len(os.sched_getaffinity(0)), "?"
+    inp = synth.generate_block_inputs(wl)
+    w = {k: O.decode(v) for k, v in inp.items()}
+    del inp
+    cfg = O.config_from_workload(wl)
+    vl = O.varlen_from_workload(wl)
+    d = wl.head_dim
+    stages = {}
+
+    def note(msg):
+        print(f"[oracle] {wl.name}: {msg}", file=sys.stderr, flush=True)
+
+    t0 = time.perf_counter()
+    mod = O.conditioning(w["t"], cfg.freq_dim, w)
+    q, k, v = O.pre_attention(cfg, vl, w["x"], w, mod)
+    stages["conditioning+pre_attention"] = time.perf_counter() - t0
+    note(f"pre-attention {stages['conditioning+pre_attention']:.1f} s")
+    if wl.is_sp_share:
+        att = synth.generate_attention_inputs(wl)
+        Ha = wl.attn_heads
+        q, k, v = (O.decode(att[n]).reshape(-1, Ha * d) for n in ("q", "k", "v"))
+        o_rows = O.decode(att["o"])
+        cu_a = wl.cu_attn()
+    else:
+        Ha, cu_a = wl.n_heads, wl.cu_seqlens()
+    o = np.zeros_like(q)
+    t1 = time.perf_counter()
+    for r in range(len(cu_a) - 1):
+        a, b = cu_a[r], cu_a[r + 1]
+        for h in range(Ha):
+            cs = slice(h * d, (h + 1) * d)
+            o[a:b, cs] = O.attention(q[a:b, cs], k[a:b, cs], v[a:b, cs], 1.0 / np.sqrt(d))
+            note(f"self-attention request {r} head {h}: {time.perf_counter() - t1:.1f} s")
+    stages["self_attention"] = time.perf_counter() - t1
+    t2 = time.perf_counter()
+    O.post_attention(cfg, vl, w["x"], o_rows if wl.is_sp_share else o, w["txt"], w, mod)
+    stages["post_attention"] = time.perf_counter() - t2
+    note(f"post-attention {stages['post_attention']:.1f} s")
+    sec = sum(stages.values())
+    fl = block_flops(wl)["total"]
+    print(json.dumps({"oracle_seconds": round(sec, 2), "workload": wl.name, "stages_s": {k: round(v, 2) for k, v in
+                      stages.items()}, "gflops_fp64": round(fl / sec / 1e9, 2), "block_flops": fl,
+                      "blas_threads": int(cores), "blas": vendor, "cpu_count": os.cpu_count(),
+                      "affinity": len(os.sched_getaffinity(0))}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -291,11 +386,21 @@ def main():
     ap.add_argument("--step", default=None, metavar="STEP_WORKLOAD",
                     help="time one whole denoising step (dit_denoise_step) at this step workload, e.g. "
                          "step_video_720p, instead of the block; prints its own JSON line")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time steps with a 1 GiB scratch write before each (inputs evicted from the caches)")
+    ap.add_argument("--oracle-seconds", action="store_true",
+                    help="only time the float64 oracle on the workload's whole block (by stages for a "
+                         "sequence-parallel share) on the host cores and print one JSON line; no GPU needed")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               f"multi-GPU sharding is designed but not built", file=sys.stderr)
         sys.exit(2)
+
+    if args.oracle_seconds:
+        import synth
+        oracle_seconds(synth.get_workload(args.workload))
+        return
 
     import numpy as np
     import torch
@@ -337,45 +442,87 @@ def main():
     o = torch.empty((T, D), dtype=tdt, device="cuda")
     cu = wl.cu_seqlens()
     stream = torch.cuda.current_stream()
+    sp = wl.is_sp_share
+    if sp:
+        # one GPU's share of sequence parallelism: self-attention over the full
+        # request lengths with the GPU's head slice (seeded q, k, v, as the
+        # all-to-all would deliver them); the rows' attention output for the
+        # post-attention steps is seeded too (the exchange back is not one GPU's work)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(13501)
+        Ha, cu_a = wl.attn_heads, wl.cu_attn()
+        qkv_a = torch.randn((cu_a[-1], 3, Ha * hd), generator=g, device="cuda").to(tdt)
+        o_a = torch.empty((cu_a[-1], Ha * hd), dtype=tdt, device="cuda")
+        o_rows = torch.randn((T, D), generator=g, device="cuda").to(tdt)
 
     def step(ev=None):
         B.block_pre_attention(cfg, w, vl, d["x"], d["t"], mod, qkv, ws)
         if ev is not None:
             ev[0].record(stream)
-        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
+        if sp:
+            B.attention_varlen(qkv_a[:, 0], qkv_a[:, 1], qkv_a[:, 2], o_a, cu_a, cu_a, Ha, hd)
+        else:
+            B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
         if ev is not None:
             ev[1].record(stream)
-        B.block_post_attention(cfg, w, vl, d["x"], o, d["txt"], mod, y, ws)
+        B.block_post_attention(cfg, w, vl, d["x"], o_rows if sp else o, d["txt"], mod, y, ws)
 
+    def new_ev():
+        return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    clocks_before = gpu_clocks()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [new_ev() for _ in range(args.steps)]
+    sevs = [new_ev() for _ in range(args.steps)]
+    start, stop = new_ev()
     torch.cuda.synchronize()
     start.record(stream)
     for i in range(args.steps):
+        sevs[i][0].record(stream)
         step(evs[i])
+        sevs[i][1].record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     attn_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    step_ms = sorted(a.elapsed_time(b) for a, b in sevs)
+    clocks_after = gpu_clocks()
 
-    # the single-call entry point, same work
-    fstart, fstop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    fstart.record(stream)
-    for _ in range(args.steps):
-        B.block_forward(cfg, w, vl, d["x"], d["t"], d["txt"], y, ws)
-    fstop.record(stream)
-    torch.cuda.synchronize()
-    fwd_ms = fstart.elapsed_time(fstop) / args.steps
+    # cold: a 1 GiB scratch write between steps evicts the inputs from the caches
+    cold = None
+    if args.cold:
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        cevs = [new_ev() for _ in range(args.steps)]
+        for i in range(args.steps):
+            scratch.fill_(i & 0xFF)
+            cevs[i][0].record(stream)
+            step()
+            cevs[i][1].record(stream)
+        torch.cuda.synchronize()
+        cold = sorted(a.elapsed_time(b) for a, b in cevs)
+        del scratch
+
+    # the single-call entry point, same work (not for a sequence-parallel share,
+    # whose attention spans rows that are not this GPU's)
+    fwd_ms = None
+    if not sp:
+        fstart, fstop = new_ev()
+        torch.cuda.synchronize()
+        fstart.record(stream)
+        for _ in range(args.steps):
+            B.block_forward(cfg, w, vl, d["x"], d["t"], d["txt"], y, ws)
+        fstop.record(stream)
+        torch.cuda.synchronize()
+        fwd_ms = fstart.elapsed_time(fstop) / args.steps
 
     fl = block_flops(wl)
     tflops = fl["total"] / (ms * 1e-3) / 1e12
     attn_flops = fl["self_attn"]
     attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
-    traffic = read_traffic()
+    traffic = read_traffic() if wl.name == "video_720p" else None   # counters were taken at 720p
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
     out = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -388,26 +535,30 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
-        "data": "synthetic (seeded; shapes of the paper's Wan2.2 720p request class, random-init weights)",
+        "data": f"synthetic (seeded; {wl.description}; random-init weights)",
         "config": {
             "workload": wl.name, "tokens": T, "requests": wl.n_req, "hidden": D, "heads": H, "head_dim": hd,
             "mlp_hidden": wl.mlp_hidden, "text_tokens": wl.n_txt, "rope_sections": list(wl.rope_sections),
             "block_flops": fl["total"], "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
-            "ms_per_step_block_forward_entry": round(fwd_ms, 3),
+            "ms_per_step_block_forward_entry": round(fwd_ms, 3) if fwd_ms is not None else None,
+            "ms_step_median": round(step_ms[len(step_ms) // 2], 3), "ms_step_min": round(step_ms[0], 3),
+            "ms_step_cold_median": round(cold[len(cold) // 2], 3) if cold else None,
+            "ms_step_cold_min": round(cold[0], 3) if cold else None,
+            "gpu_clocks_before": clocks_before, "gpu_clocks_after": clocks_after,
         },
         "roofline": {
-            "kernel": "attn_fwd_bf16 (self-attention)",
+            "kernel": "attn_fwd_bf16 (self-attention)" if wl.dtype == "bf16" else "attn_fwd_f32 (self-attention)",
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
-            "peak": PEAK_BF16_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+            "frac": round(attn_tflops / peak, 4),
             "traffic": traffic,
             "flops_per_launch": attn_flops,
             "ms_per_launch": round(attn_ms, 3),
         },
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not sp:   # a share's oracle timing: --oracle-seconds (by stages)
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(wl)
         print(f"[bench] cpu baseline took {time.time() - t0:.1f} s", file=sys.stderr, flush=True)

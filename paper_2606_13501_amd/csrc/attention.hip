@@ -124,14 +124,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // slot t % kRing holds K(t) (first 8 KiB) and V(t)
   __shared__ __attribute__((aligned(1024))) char smem[kRing * kSlotBytes];
 
-  // ---- work item: XCD-contiguous numbering, requests longest first
-  const int nb = gridDim.x;
-  const int b = blockIdx.x;
-  const int w = (b % kXcds) * (nb / kXcds) + b / kXcds;
-  if (w >= work.prefix[work.n_req]) return;
-  int r = 0;
-  while (w >= work.prefix[r + 1]) ++r;
-  const int local = w - work.prefix[r];
+  // ---- work item.  Workgroups are dispatched to the XCDs round-robin, so
+  // workgroup b runs on XCD b % 8 as that XCD's (b / 8)-th.  Each XCD takes
+  // the same contiguous eighth of every request's items (head-major, requests
+  // longest first): the long requests' work is spread over all XCDs, and the
+  // query tiles of one head stay together on one XCD, sharing its K/V in L2.
+  const int xcd = blockIdx.x % kXcds;
+  int j = blockIdx.x / kXcds;
+  int r = 0, local = -1;
+  for (; r < work.n_req; ++r) {
+    const int n_r = work.prefix[r + 1] - work.prefix[r];
+    const int lo = xcd * n_r / kXcds, hi = (xcd + 1) * n_r / kXcds;
+    if (j < hi - lo) {
+      local = lo + j;
+      break;
+    }
+    j -= hi - lo;
+  }
+  if (local < 0) return;
   const int head = local / work.tiles_q[r];
   const int qt = local - head * work.tiles_q[r];
   const int q0 = work.q_start[r] + qt * BQ;
@@ -550,7 +560,18 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
   }
   const int items = w.prefix[n];
   if (items == 0) return hipSuccess;
-  const int grid = (items + kXcds - 1) / kXcds * kXcds;
+  if (items > (1 << 27)) return hipErrorInvalidValue;   // keeps xcd * n_r in range
+  // each XCD's share of every request (see the kernel); the grid covers the largest
+  int per_xcd = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    int len = 0;
+    for (int i = 0; i < n; ++i) {
+      const int n_r = w.prefix[i + 1] - w.prefix[i];
+      len += (x + 1) * n_r / kXcds - x * n_r / kXcds;
+    }
+    per_xcd = len > per_xcd ? len : per_xcd;
+  }
+  const int grid = per_xcd * kXcds;
   const float scale_log2 = p.scale * 1.4426950408889634f;
   attn_fwd_bf16<<<grid, kThreads, 0, s>>>((const bf16*)p.q, (const bf16*)p.k, (const bf16*)p.v,
                                           (bf16*)p.o, p.q_stride, p.k_stride, p.v_stride, p.o_stride,
