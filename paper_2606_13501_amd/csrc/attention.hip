@@ -490,36 +490,55 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
 
 // ------------------------------------------------------------------- fp32
 
+// One thread per (query row, head); HD is a compile-time head size, so q and
+// the output accumulator stay in registers and K, V rows are read as 16-byte
+// vectors.  Online softmax in fp32.
+template <int HD>
 __global__ __launch_bounds__(64) void attn_fwd_f32(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
-    float* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads, int head_dim,
-    float scale, ReqTable cq, ReqTable ck, int n_q) {
+    float* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads, float scale,
+    ReqTable cq, ReqTable ck, int n_q) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= n_q * n_heads) return;
   const int row = idx / n_heads;
   const int head = idx - row * n_heads;
   const int r = find_req(cq.cu, cq.n_req, row);
   const int kb = ck.cu[r], ke = ck.cu[r + 1];
-  const float* q = Q + (int64_t)row * qs + head * head_dim;
+  f32x4 q[HD / 4], acc[HD / 4];
+  const f32x4* qp = reinterpret_cast<const f32x4*>(Q + (int64_t)row * qs + head * HD);
+#pragma unroll
+  for (int e = 0; e < HD / 4; ++e) {
+    q[e] = qp[e];
+    acc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   float m = -INFINITY, l = 0.f;
-  float acc[128];
-  for (int e = 0; e < head_dim; ++e) acc[e] = 0.f;
   for (int j = kb; j < ke; ++j) {
-    const float* k = K + (int64_t)j * ks + head * head_dim;
-    float s = 0.f;
-    for (int e = 0; e < head_dim; ++e) s = fmaf(q[e], k[e], s);
-    s *= scale;
-    float m_new = fmaxf(m, s);
-    float a = expf(m - m_new);
-    float p = expf(s - m_new);
+    const f32x4* kp = reinterpret_cast<const f32x4*>(K + (int64_t)j * ks + head * HD);
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int e = 0; e < HD / 4; e += 2) {
+      const f32x4 a = kp[e], b = kp[e + 1];
+      s0 = fmaf(q[e][0], a[0], fmaf(q[e][1], a[1], fmaf(q[e][2], a[2], fmaf(q[e][3], a[3], s0))));
+      s1 = fmaf(q[e + 1][0], b[0], fmaf(q[e + 1][1], b[1], fmaf(q[e + 1][2], b[2], fmaf(q[e + 1][3], b[3], s1))));
+    }
+    const float s = (s0 + s1) * scale;
+    const float m_new = fmaxf(m, s);
+    const float a = expf(m - m_new);
+    const float p = expf(s - m_new);
     l = l * a + p;
-    const float* v = V + (int64_t)j * vs + head * head_dim;
-    for (int e = 0; e < head_dim; ++e) acc[e] = acc[e] * a + p * v[e];
+    const f32x4* vp = reinterpret_cast<const f32x4*>(V + (int64_t)j * vs + head * HD);
+#pragma unroll
+    for (int e = 0; e < HD / 4; ++e) {
+      const f32x4 v = vp[e];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[e][c] = fmaf(p, v[c], acc[e][c] * a);
+    }
     m = m_new;
   }
-  float* o = O + (int64_t)row * os + head * head_dim;
+  f32x4* op = reinterpret_cast<f32x4*>(O + (int64_t)row * os + head * HD);
   const float inv = ke > kb ? 1.0f / l : 0.f;
-  for (int e = 0; e < head_dim; ++e) o[e] = acc[e] * inv;
+#pragma unroll
+  for (int e = 0; e < HD / 4; ++e) op[e] = acc[e] * inv;
 }
 
 }  // namespace
@@ -530,9 +549,14 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
     const int n_q = p.cq.cu[n_req];
     if (n_q == 0) return hipSuccess;
     const int total = n_q * p.n_heads;
-    attn_fwd_f32<<<(total + 63) / 64, 64, 0, s>>>(
-        (const float*)p.q, (const float*)p.k, (const float*)p.v, (float*)p.o, p.q_stride, p.k_stride,
-        p.v_stride, p.o_stride, p.n_heads, p.head_dim, p.scale, p.cq, p.ck, n_q);
+    if (p.head_dim == 64)
+      attn_fwd_f32<64><<<(total + 63) / 64, 64, 0, s>>>(
+          (const float*)p.q, (const float*)p.k, (const float*)p.v, (float*)p.o, p.q_stride, p.k_stride,
+          p.v_stride, p.o_stride, p.n_heads, p.scale, p.cq, p.ck, n_q);
+    else
+      attn_fwd_f32<128><<<(total + 63) / 64, 64, 0, s>>>(
+          (const float*)p.q, (const float*)p.k, (const float*)p.v, (float*)p.o, p.q_stride, p.k_stride,
+          p.v_stride, p.o_stride, p.n_heads, p.scale, p.cq, p.ck, n_q);
     return hipGetLastError();
   }
   // requests with queries, longest key range first (their tiles do the most work)
