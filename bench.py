@@ -253,6 +253,96 @@ def run_step(args):
     print(json.dumps(out), flush=True)
 
 
+XGMI_LINK_GBS = 153.0   # one xGMI link, one direction (MI355X: 7 links per GPU, one to each peer)
+
+
+def run_cost_table(args):
+    """Latency of one denoising step per (request class, sequence-parallel
+    degree): one GPU's share of a block, timed on this GPU (per-token stages on
+    its ceil(n/d) rows with all heads, self-attention over all n rows with H/d
+    heads, seeded operands), times the model's depth, plus a model of the two
+    all-to-alls per block (q, k, v out and o back: 4 (n/d) D bf16 values per
+    GPU, 1/d of it to each peer over its own link).  Prints one JSON line per
+    entry and a final line with the whole table."""
+    import torch
+    import synth
+    import paper_2606_13501_amd.binding as B
+    g = torch.Generator(device="cuda")
+    g.manual_seed(13501)
+    stream = torch.cuda.current_stream()
+    table = {}
+    for model in ("video", "image"):
+        D, H, hd, Dff, F, sec, n_blocks, L = synth.MODEL_SHAPES[model]
+        classes = [c for c in synth.REQUEST_CLASSES.values() if c.model == model]
+        n_max = max(c.tokens for c in classes)
+
+        def normal(shape, std=1.0, mean=0.0):
+            return (torch.randn(shape, generator=g, device="cuda") * std + mean).to(torch.bfloat16)
+
+        shapes = {"w_t1": (D, F), "b_t1": (D,), "w_t2": (D, D), "b_t2": (D,), "w_ada": (6 * D, D), "b_ada": (6 * D,),
+                  "w_qkv": (3 * D, D), "b_qkv": (3 * D,), "g_q": (hd,), "g_k": (hd,), "w_o": (D, D), "b_o": (D,),
+                  "g_ca": (D,), "b_ca": (D,), "w_cq": (D, D), "b_cq": (D,), "w_ckv": (2 * D, D), "b_ckv": (2 * D,),
+                  "g_cq": (hd,), "g_ck": (hd,), "w_co": (D, D), "b_co": (D,), "w_up": (Dff, D), "b_up": (Dff,),
+                  "w_dn": (D, Dff), "b_dn": (D,)}
+        wd = {n: normal(shp, 0.02, 1.0 if n.startswith("g_") else 0.0) for n, shp in shapes.items()}
+        w = B.make_weights(wd)
+        x = normal((n_max, D))
+        txt = normal((L, D))
+        t = torch.rand((1,), generator=g, device="cuda") * 1000.0
+        cfg = B.BlockConfig(D, H, hd, Dff, F, sec, torch.bfloat16)
+        for c in classes:
+            for deg in synth.SP_DEGREES:
+                wl = synth.share_workload(c, deg)
+                T = wl.rows[0]
+                vl = B.Varlen([0, T], [0, L], [c.grid])
+                ws = torch.empty(B.block_workspace_size(cfg, vl), dtype=torch.uint8, device="cuda")
+                mod = torch.empty((1, 6, D), dtype=torch.float32, device="cuda")
+                qkv = torch.empty((T, 3 * D), dtype=torch.bfloat16, device="cuda")
+                o = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+                y = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+                xs = x[:T]
+                if deg > 1:
+                    Ha, n = H // deg, c.tokens
+                    qkv_a = normal((n, 3, Ha * hd))
+                    o_a = torch.empty((n, Ha * hd), dtype=torch.bfloat16, device="cuda")
+                    o_rows = normal((T, D))
+
+                def share():
+                    B.block_pre_attention(cfg, w, vl, xs, t, mod, qkv, ws)
+                    if deg > 1:
+                        B.attention_varlen(qkv_a[:, 0], qkv_a[:, 1], qkv_a[:, 2], o_a, [0, c.tokens], [0, c.tokens],
+                                           Ha, hd)
+                    else:
+                        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, [0, T], [0, T], H, hd)
+                    B.block_post_attention(cfg, w, vl, xs, o_rows if deg > 1 else o, txt, mod, y, ws)
+
+                for _ in range(args.warmup):
+                    share()
+                evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                       for _ in range(args.steps)]
+                torch.cuda.synchronize()
+                for a, b in evs:
+                    a.record(stream)
+                    share()
+                    b.record(stream)
+                torch.cuda.synchronize()
+                ms = sorted(a.elapsed_time(b) for a, b in evs)
+                comm = 0.0 if deg == 1 else 4.0 * T * D * 2 / deg / (XGMI_LINK_GBS * 1e9) * 1e3
+                step_ms = n_blocks * (ms[len(ms) // 2] + comm)
+                table[(c.name, deg)] = step_ms
+                print(json.dumps({"cost_entry": c.name, "tokens": c.tokens, "degree": deg, "rows": T,
+                                  "attn_heads": H // deg, "block_ms_median": round(ms[len(ms) // 2], 4),
+                                  "block_ms_min": round(ms[0], 4), "comm_ms_model": round(comm, 4),
+                                  "blocks": n_blocks, "step_ms": round(step_ms, 3)}), flush=True)
+                del ws, qkv, o, y
+                if deg > 1:
+                    del qkv_a, o_a, o_rows
+        del wd, w, x
+        torch.cuda.empty_cache()
+    print(json.dumps({"cost_table_step_ms": {f"{k[0]}@{k[1]}": round(v, 3) for k, v in table.items()},
+                      "degrees": list(synth.SP_DEGREES), "steps": args.steps, "warmup": args.warmup}), flush=True)
+
+
 def profile_kernel(args, wl):
     """One kernel alone, args.steps times, for counter collection."""
     import torch
@@ -391,6 +481,9 @@ def main():
     ap.add_argument("--oracle-seconds", action="store_true",
                     help="only time the float64 oracle on the workload's whole block (by stages for a "
                          "sequence-parallel share) on the host cores and print one JSON line; no GPU needed")
+    ap.add_argument("--cost-table", action="store_true",
+                    help="measure the denoising-step cost table (request class x sequence-parallel degree) "
+                         "from one GPU's share of a block and print it")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -414,6 +507,9 @@ def main():
     torch.cuda.set_device(0)
     if args.step:
         run_step(args)
+        return
+    if args.cost_table:
+        run_cost_table(args)
         return
     wl = synth.get_workload(args.workload)
     if args.profile_kernel:

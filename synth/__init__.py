@@ -6,6 +6,7 @@ read the exact same stored bits from here.
 """
 from .workloads import (
     Workload, WORKLOADS, get_workload, ModelWorkload, MODEL_WORKLOADS, get_model_workload,
+    RequestClass, REQUEST_CLASSES, MODEL_SHAPES, SP_DEGREES, share_workload,
 )
 from .gen import (
     bf16_bits, generate_block_inputs, generate_tensor, TensorSpec, draw,
@@ -18,5 +19,6 @@ __all__ = [
     "generate_tensor", "TensorSpec", "block_tensor_specs",
     "generate_attention_inputs", "generate_sampled_rows", "draw",
     "ModelWorkload", "MODEL_WORKLOADS", "get_model_workload", "model_tensor_specs",
-    "generate_model_inputs", "MODEL_WEIGHT_NAMES",
+    "generate_model_inputs", "MODEL_WEIGHT_NAMES", "RequestClass", "REQUEST_CLASSES", "MODEL_SHAPES",
+    "SP_DEGREES", "share_workload",
 ]

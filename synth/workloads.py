@@ -163,3 +163,54 @@ def get_model_workload(name: str) -> ModelWorkload:
         return MODEL_WORKLOADS[name]
     except KeyError:
         raise KeyError(f"unknown step workload {name!r}; known: {sorted(MODEL_WORKLOADS)}") from None
+
+
+# Request classes of the paper's evaluation (section 6.1): Wan2.2 videos S/M/L
+# (480x832 with 49 frames, 480x832 with 81 frames, 720x1280 with 81 frames) and
+# Qwen-Image images S/M/L (512^2, 1024^2, 1536^2), with their SLO multipliers
+# alpha.  Token counts use the same VAE/patch reading as the block workloads
+# (49 frames -> 13 latent frames).  `model` names the block shape of the model
+# that serves the class and `n_blocks` its depth.
+@dataclass(frozen=True)
+class RequestClass:
+    name: str
+    model: str          # "video" (D 5120, 40 x 128 heads) or "image" (D 3072, 24 x 128 heads)
+    grid: Tuple[int, int, int]
+    alpha: float
+    n_steps: int = 50
+
+    @property
+    def tokens(self) -> int:
+        return self.grid[0] * self.grid[1] * self.grid[2]
+
+
+MODEL_SHAPES = {
+    # hidden, heads, head_dim, mlp_hidden, freq_dim, rope sections, blocks, text tokens
+    "video": (5120, 40, 128, 13824, 5120, (44, 42, 42), 40, 512),
+    "image": (3072, 24, 128, 12288, 3072, (0, 64, 64), 60, 512),
+}
+
+REQUEST_CLASSES: Dict[str, RequestClass] = {c.name: c for c in [
+    RequestClass("video_S", "video", (13, 30, 52), 2.0),
+    RequestClass("video_M", "video", (21, 30, 52), 2.5),
+    RequestClass("video_L", "video", (21, 45, 80), 3.5),
+    RequestClass("image_S", "image", (1, 32, 32), 1.5),
+    RequestClass("image_M", "image", (1, 64, 64), 2.0),
+    RequestClass("image_L", "image", (1, 96, 96), 6.0),
+]}
+SP_DEGREES = (1, 2, 4, 8)
+
+
+def share_workload(cls: RequestClass, degree: int) -> Workload:
+    """One GPU's share of a class's block at sequence-parallel degree `degree`:
+    per-token stages on the first ceil(n/degree) rows with all heads,
+    self-attention over all n rows with heads/degree heads."""
+    D, H, d, Dff, F, sec, _, L = MODEL_SHAPES[cls.model]
+    n = cls.tokens
+    rows = -(-n // degree)
+    return Workload(name=f"{cls.name}.sp{degree}", wid=100 + degree, dtype="bf16", hidden=D, n_heads=H,
+                    head_dim=d, mlp_hidden=Dff, freq_dim=F, rope_sections=sec, grids=(cls.grid,), rows=(rows,),
+                    txt_len=L, attn_heads=H // degree if degree > 1 else None,
+                    attn_rows=(n,) if degree > 1 else None,
+                    description=f"{cls.name} at SP degree {degree}: {rows} of {n} rows, "
+                                f"{H // degree} of {H} heads in self-attention")
