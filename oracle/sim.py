@@ -148,7 +148,7 @@ def simulate(n_ranks: int, degrees: Sequence[int], cost_us: Sequence[Sequence[in
                         start(i, now, g, j)
         else:
             order = sorted([i for i in range(n) if ready[i]],
-                           key=lambda q: (dl[q] < 0, dl[q], arrival[q], q))
+                           key=lambda q: (dl[q] < 0, max(dl[q], 0), arrival[q], q))
             for i in order:
                 f = len(free_ranks)
                 if f == 0:

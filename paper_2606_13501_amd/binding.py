@@ -75,6 +75,25 @@ class CModelWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in MODEL_FIELDS] + [("blocks", ctypes.POINTER(CWeights))]
 
 
+class CSimConfig(ctypes.Structure):
+    _fields_ = [("n_ranks", ctypes.c_int), ("n_degrees", ctypes.c_int), ("degrees", ctypes.POINTER(ctypes.c_int32)),
+                ("n_classes", ctypes.c_int), ("cost_us", ctypes.POINTER(ctypes.c_int64)), ("policy", ctypes.c_int),
+                ("group_size", ctypes.c_int)]
+
+
+class CSimTrace(ctypes.Structure):
+    _fields_ = [("n_req", ctypes.c_int64), ("arrival_us", ctypes.POINTER(ctypes.c_int64)),
+                ("cls", ctypes.POINTER(ctypes.c_int32)), ("n_steps", ctypes.POINTER(ctypes.c_int32)),
+                ("deadline_us", ctypes.POINTER(ctypes.c_int64))]
+
+
+class CSimResult(ctypes.Structure):
+    _fields_ = [("finish_us", ctypes.POINTER(ctypes.c_int64)), ("first_start_us", ctypes.POINTER(ctypes.c_int64)),
+                ("dispatches", ctypes.POINTER(ctypes.c_int64)), ("events", ctypes.c_int64)]
+
+
+SIM_FCFS_GROUPS, SIM_SRTF_GROUPS, SIM_EDF_BESTFIT = 0, 1, 2
+
 _lib = None
 
 
@@ -108,6 +127,7 @@ def lib() -> ctypes.CDLL:
         "dit_denoise_step": (i32, [PM, PMW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_patchify": (i32, [PM, PV, vp, vp, vp]),
         "dit_unpatchify_euler": (i32, [PM, PV, vp, vp, vp, vp, vp]),
+        "dit_simulate": (i32, [ctypes.POINTER(CSimConfig), ctypes.POINTER(CSimTrace), ctypes.POINTER(CSimResult)]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -125,7 +145,8 @@ def exported_symbols() -> Sequence[str]:
                         "dit_block_post_attention", "dit_timestep_modulation", "dit_attention_varlen",
                         "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
-                        "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_status_string",
+                        "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
+                        "dit_status_string",
                         "dit_last_error", "dit_abi_version")]
 
 
@@ -334,3 +355,29 @@ def patchify(cfg: ModelConfig, vl: Varlen, latent, tokens, stream=None):
 def unpatchify_euler(cfg: ModelConfig, vl: Varlen, latent, v, dt, latent_out, stream=None):
     _check(lib().dit_unpatchify_euler(ctypes.byref(cfg.c), ctypes.byref(vl.c), _ptr(latent), _ptr(v), _ptr(dt),
                                       _ptr(latent_out), _stream(stream)), "dit_unpatchify_euler")
+
+
+# ------------------------------------------------------------ the simulator
+
+
+def simulate(n_ranks: int, degrees, cost_us, policy: int, group_size: int, arrival_us, cls, n_steps,
+             deadline_us=None) -> Dict[str, object]:
+    """dit_simulate on host arrays.  cost_us: [n_classes][n_degrees] integer
+    microseconds.  Returns finish_us, first_start_us (int64 arrays),
+    dispatches (per degree) and events."""
+    deg = _i32(degrees)
+    cost = np.ascontiguousarray(np.asarray(cost_us, dtype=np.int64))
+    arr = np.ascontiguousarray(np.asarray(arrival_us, dtype=np.int64))
+    cl = _i32(cls)
+    st = _i32(n_steps)
+    dl = np.ascontiguousarray(np.asarray(deadline_us, dtype=np.int64)) if deadline_us is not None else None
+    n = len(arr)
+    fin = np.zeros(n, dtype=np.int64)
+    first = np.zeros(n, dtype=np.int64)
+    disp = np.zeros(len(deg), dtype=np.int64)
+    p64 = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if a is not None else None
+    cfg = CSimConfig(int(n_ranks), len(deg), _pi(deg), int(cost.shape[0]), p64(cost), int(policy), int(group_size))
+    tr = CSimTrace(n, p64(arr), _pi(cl), _pi(st), p64(dl))
+    res = CSimResult(p64(fin), p64(first), p64(disp), 0)
+    _check(lib().dit_simulate(ctypes.byref(cfg), ctypes.byref(tr), ctypes.byref(res)), "dit_simulate")
+    return {"finish": fin, "first_start": first, "dispatches": disp, "events": int(res.events)}

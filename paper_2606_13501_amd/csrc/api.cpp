@@ -493,6 +493,11 @@ dit_status run_cond_parts(const dit_block_config* c, int n_req, const float* t, 
 
 }  // namespace
 
+namespace dit {
+// Sets this thread's dit_last_error() message (used by the other C-ABI units).
+void set_last_error(const std::string& msg) { g_last_error = msg; }
+}  // namespace dit
+
 extern "C" {
 
 int dit_abi_version(void) { return DIT_ABI_VERSION; }

@@ -21,7 +21,7 @@ def _lib():
 
 
 def header_functions():
-    txt = open(HEADER).read()
+    txt = open(HEADER).read() + open(os.path.join(ROOT, "include", "dit_sim.h")).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
     return sorted(set(re.findall(r"\b(dit_[a-z_0-9]+)\s*\(", txt)))
 

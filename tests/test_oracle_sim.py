@@ -30,7 +30,7 @@ MUTANTS = {
                            "key=lambda q: (-(n_steps[q] - started[q]) * cost(q, g), arrival[q], q))"),
     "srtf_counts_done_not_started": ("key=lambda q: ((n_steps[q] - started[q]) * cost(q, g)",
                                      "key=lambda q: ((n_steps[q] - done[q]) * cost(q, g) * 0 + arrival[q] * 0"),
-    "edf_ignores_deadline": ("key=lambda q: (dl[q] < 0, dl[q], arrival[q], q))",
+    "edf_ignores_deadline": ("key=lambda q: (dl[q] < 0, max(dl[q], 0), arrival[q], q))",
                              "key=lambda q: (arrival[q], q))"),
     "edf_largest_meeting": ("d = meet[0]", "d = meet[-1]"),
     "edf_no_regrowth": ("d = min(allowed, key=lambda x: (now + rem * cost(i, x), x))", "d = allowed[0]"),
