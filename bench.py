@@ -343,6 +343,62 @@ def run_cost_table(args):
                       "degrees": list(synth.SP_DEGREES), "steps": args.steps, "warmup": args.warmup}), flush=True)
 
 
+SIM_POLICIES = [("FCFS-SP1", 0, 1), ("FCFS-SP8", 0, 8), ("SRTF-SP1", 1, 1), ("SRTF-SP8", 1, 8), ("EDF-bestfit", 2, 1)]
+
+
+def run_simulate(args):
+    """Replay seeded traces of the paper's two workloads (mixed, foreground
+    burst) for the video and the image classes on 8 ranks under each policy,
+    with step costs from the measured cost table, in the library's simulator;
+    the simulator oracle replays the same traces beside it for its timing.
+    Prints one JSON line per (model, workload) and one with the simulators'
+    event rates."""
+    import numpy as np
+    import synth
+    import paper_2606_13501_amd.binding as B
+    from oracle import sim as S
+    step_ms = synth.read_cost_table(os.path.join(ROOT, "profiles", "step_cost_table.md"))
+    degrees = list(synth.SP_DEGREES)
+    G = 8
+    lib_ev = lib_s = ora_ev = ora_s = 0.0
+    for model, duration, allowance_s in (("video", 3600.0, 5.0), ("image", 600.0, 1.0)):
+        for kind in ("mixed", "burst"):
+            tr = synth.make_trace(kind, model, step_ms, G, duration, args.load, seed=0)
+            cost = synth.cost_matrix(step_ms, tr["classes"], degrees)
+            arr = np.asarray(tr["arrival_us"], dtype=np.int64)
+            dl = np.asarray(tr["deadline_us"], dtype=np.int64)
+            line = {"simulate": f"{model}/{kind}", "ranks": G, "requests": len(arr), "load": args.load,
+                    "duration_s": duration, "policies": {}}
+            for name, pol, grp in SIM_POLICIES:
+                t0 = time.perf_counter()
+                r = B.simulate(G, degrees, cost, pol, grp, arr, tr["cls"], tr["n_steps"], dl)
+                lib_s += time.perf_counter() - t0
+                lib_ev += r["events"]
+                if args.sim_oracle:
+                    t0 = time.perf_counter()
+                    ro = S.simulate(G, degrees, cost, pol, grp, tr["arrival_us"], tr["cls"], tr["n_steps"],
+                                    tr["deadline_us"])
+                    ora_s += time.perf_counter() - t0
+                    ora_ev += ro["events"]
+                    if ro["finish"] != r["finish"].tolist():
+                        raise RuntimeError(f"simulator and oracle differ on {model}/{kind} {name}")
+                lat = (r["finish"] - arr) / 1e6
+                met = r["finish"] <= dl + int(allowance_s * 1e6)
+                line["policies"][name] = {
+                    "slo_attainment": round(float(met.mean()), 4),
+                    "mean_latency_s": round(float(lat.mean()), 2),
+                    "p99_latency_s": round(float(np.percentile(lat, 99)), 2),
+                    "makespan_s": round(float(r["finish"].max()) / 1e6, 1),
+                    "steps_per_degree": dict(zip([str(d) for d in degrees], r["dispatches"].tolist())),
+                }
+            print(json.dumps(line), flush=True)
+    rates = {"simulator_events_per_s": round(lib_ev / lib_s), "events": int(lib_ev)}
+    if args.sim_oracle:
+        rates["oracle_events_per_s"] = round(ora_ev / ora_s)
+        rates["speedup"] = round((lib_ev / lib_s) / (ora_ev / ora_s), 1)
+    print(json.dumps(rates), flush=True)
+
+
 def profile_kernel(args, wl):
     """One kernel alone, args.steps times, for counter collection."""
     import torch
@@ -484,12 +540,20 @@ def main():
     ap.add_argument("--cost-table", action="store_true",
                     help="measure the denoising-step cost table (request class x sequence-parallel degree) "
                          "from one GPU's share of a block and print it")
+    ap.add_argument("--simulate", action="store_true",
+                    help="replay seeded traces under each scheduling policy with the measured cost table "
+                         "(CPU only) and print the policies' SLO attainment and latency")
+    ap.add_argument("--sim-oracle", action="store_true", help="with --simulate: also time the simulator oracle")
+    ap.add_argument("--load", type=float, default=0.8, help="with --simulate: offered load (fraction of capacity)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               f"multi-GPU sharding is designed but not built", file=sys.stderr)
         sys.exit(2)
 
+    if args.simulate:
+        run_simulate(args)
+        return
     if args.oracle_seconds:
         import synth
         oracle_seconds(synth.get_workload(args.workload))
