@@ -94,6 +94,27 @@ class CSimResult(ctypes.Structure):
 
 SIM_FCFS_GROUPS, SIM_SRTF_GROUPS, SIM_EDF_BESTFIT = 0, 1, 2
 
+MIG_SHARDED, MIG_REPLICATED, MIG_METADATA = 0, 1, 2
+MIG_MAX_DIMS = 4
+
+
+class CMigSlice(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("start", ctypes.c_int64 * MIG_MAX_DIMS),
+                ("end", ctypes.c_int64 * MIG_MAX_DIMS)]
+
+
+class CMigField(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("n_dims", ctypes.c_int), ("shape", ctypes.c_int64 * MIG_MAX_DIMS),
+                ("elem_bytes", ctypes.c_int), ("n_src", ctypes.c_int), ("src", ctypes.POINTER(CMigSlice)),
+                ("n_dst", ctypes.c_int), ("dst", ctypes.POINTER(CMigSlice))]
+
+
+class CMigEntry(ctypes.Structure):
+    _fields_ = [("src_index", ctypes.c_int32), ("dst_index", ctypes.c_int32), ("src_rank", ctypes.c_int32),
+                ("dst_rank", ctypes.c_int32), ("src_off", ctypes.c_int64 * MIG_MAX_DIMS),
+                ("dst_off", ctypes.c_int64 * MIG_MAX_DIMS), ("extent", ctypes.c_int64 * MIG_MAX_DIMS),
+                ("bytes", ctypes.c_int64)]
+
 _lib = None
 
 
@@ -128,6 +149,10 @@ def lib() -> ctypes.CDLL:
         "dit_patchify": (i32, [PM, PV, vp, vp, vp]),
         "dit_unpatchify_euler": (i32, [PM, PV, vp, vp, vp, vp, vp]),
         "dit_simulate": (i32, [ctypes.POINTER(CSimConfig), ctypes.POINTER(CSimTrace), ctypes.POINTER(CSimResult)]),
+        "dit_migration_plan": (i32, [ctypes.POINTER(CMigField), ctypes.POINTER(CMigEntry), i64,
+                                     ctypes.POINTER(ctypes.c_int64)]),
+        "dit_migration_execute": (i32, [ctypes.POINTER(CMigField), ctypes.POINTER(CMigEntry), i64,
+                                        ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -146,6 +171,7 @@ def exported_symbols() -> Sequence[str]:
                         "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
                         "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
+                        "dit_migration_plan", "dit_migration_execute",
                         "dit_status_string",
                         "dit_last_error", "dit_abi_version")]
 
@@ -381,3 +407,46 @@ def simulate(n_ranks: int, degrees, cost_us, policy: int, group_size: int, arriv
     res = CSimResult(p64(fin), p64(first), p64(disp), 0)
     _check(lib().dit_simulate(ctypes.byref(cfg), ctypes.byref(tr), ctypes.byref(res)), "dit_simulate")
     return {"finish": fin, "first_start": first, "dispatches": disp, "events": int(res.events)}
+
+
+# ------------------------------------------------------------ migration
+
+
+class MigField:
+    """Python view of dit_mig_field; keeps its slice arrays alive.  src, dst:
+    lists of (rank, start, end) boxes in global coordinates."""
+
+    def __init__(self, kind: int, shape, elem_bytes: int, src, dst):
+        self.src = (CMigSlice * max(1, len(src)))()
+        self.dst = (CMigSlice * max(1, len(dst)))()
+        for arr, sl in ((self.src, src), (self.dst, dst)):
+            for k, (rank, a, b) in enumerate(sl):
+                arr[k].rank = int(rank)
+                for d in range(len(shape)):
+                    arr[k].start[d], arr[k].end[d] = int(a[d]), int(b[d])
+        self.c = CMigField()
+        self.c.kind, self.c.n_dims, self.c.elem_bytes = int(kind), len(shape), int(elem_bytes)
+        for d in range(len(shape)):
+            self.c.shape[d] = int(shape[d])
+        self.c.n_src, self.c.src = len(src), ctypes.cast(self.src, ctypes.POINTER(CMigSlice))
+        self.c.n_dst, self.c.dst = len(dst), ctypes.cast(self.dst, ctypes.POINTER(CMigSlice))
+
+
+def migration_plan(field: MigField):
+    """The plan of a field as a ctypes array of CMigEntry (sized by a first call)."""
+    n = ctypes.c_int64(0)
+    st = lib().dit_migration_plan(ctypes.byref(field.c), None, 0, ctypes.byref(n))
+    if st not in (DIT_OK, DIT_ERR_WORKSPACE):
+        _check(st, "dit_migration_plan")
+    entries = (CMigEntry * max(1, n.value))()
+    _check(lib().dit_migration_plan(ctypes.byref(field.c), entries, n.value, ctypes.byref(n)), "dit_migration_plan")
+    return entries, n.value
+
+
+def migration_execute(field: MigField, entries, n: int, src_bufs, dst_bufs, stream=None):
+    """Apply a plan on the current device: src_bufs / dst_bufs are tensors
+    holding the slices densely, in the order of the field's slices."""
+    sp = (ctypes.c_void_p * max(1, len(src_bufs)))(*[t.data_ptr() for t in src_bufs])
+    dp = (ctypes.c_void_p * max(1, len(dst_bufs)))(*[t.data_ptr() for t in dst_bufs])
+    _check(lib().dit_migration_execute(ctypes.byref(field.c), entries, n, sp, dp, _stream(stream)),
+           "dit_migration_execute")

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libditblock.so")
 
-SOURCES = ["gemm.hip", "attention.hip", "rowwise.hip", "latent.hip", "api.cpp", "sim.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "rowwise.hip", "latent.hip", "api.cpp", "sim.cpp", "migrate.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC,

@@ -21,7 +21,7 @@ def _lib():
 
 
 def header_functions():
-    txt = open(HEADER).read() + open(os.path.join(ROOT, "include", "dit_sim.h")).read()
+    txt = "".join(open(os.path.join(ROOT, "include", h)).read() for h in ("dit_block.h", "dit_sim.h", "dit_migrate.h"))
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
     return sorted(set(re.findall(r"\b(dit_[a-z_0-9]+)\s*\(", txt)))
 
