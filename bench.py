@@ -399,6 +399,63 @@ def run_simulate(args):
     print(json.dumps(rates), flush=True)
 
 
+def run_migrate(args):
+    """Rebuild the 720p video latent (fp32, channel-major 16 x 21 x 90 x 160,
+    sharded by token rows, i.e. along its height in bands of whole token rows)
+    from one sequence-parallel degree to another with the migration planner,
+    executing the plan on this GPU (device buffers stand in for the ranks).
+    Prints, per degree pair, the plan's entries and bytes, the device time of
+    the execution and a model of the same transfers over xGMI (each entry one
+    point-to-point transfer; a rank's sends share its link to the peer)."""
+    import torch
+    import paper_2606_13501_amd.binding as B
+    from collections import defaultdict
+    C, FL, HL, WL, ph = 16, 21, 90, 160, 2
+    H = HL // ph
+    g = torch.randn(C, FL, HL, WL, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def layout(d, base):
+        # rank i owns token rows (f, h) with f*H + h in its ceil-split of F*H: here, h bands per frame
+        # collapse to bands of the height that cover whole token rows, for every frame at once
+        out = []
+        for i in range(d):
+            a, b = -(-H * i // d), -(-H * (i + 1) // d)
+            out.append((base + i, [0, 0, a * ph, 0], [C, FL, b * ph, WL]))
+        return out
+
+    for d1 in (1, 2, 4, 8):
+        for d2 in (1, 2, 4, 8):
+            if d1 == d2:
+                continue
+            src, dst = layout(d1, 0), layout(d2, 16)
+            f = B.MigField(B.MIG_SHARDED, (C, FL, HL, WL), 4, src, dst)
+            entries, n = B.migration_plan(f)
+            sb = [g[:, :, s[2]:e[2], :].contiguous() for _, s, e in src]
+            db = [torch.empty(C, FL, e[2] - s[2], WL, device="cuda") for _, s, e in dst]
+            for _ in range(args.warmup):
+                B.migration_execute(f, entries, n, sb, db)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for _ in range(args.steps):
+                B.migration_execute(f, entries, n, sb, db)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / args.steps
+            moved = sum(entries[k].bytes for k in range(n))
+            remote = defaultdict(int)
+            for k in range(n):
+                if entries[k].src_rank != entries[k].dst_rank:
+                    remote[(entries[k].src_rank, entries[k].dst_rank)] += entries[k].bytes
+            xgmi_ms = max(remote.values()) / (XGMI_LINK_GBS * 1e9) * 1e3 if remote else 0.0
+            print(json.dumps({"migrate": f"sp{d1}->sp{d2}", "entries": n, "bytes": moved,
+                              "device_ms": round(ms, 4), "device_GBps": round(2 * moved / ms / 1e6, 1),
+                              "xgmi_model_ms": round(xgmi_ms, 4)}), flush=True)
+            for t in sb + db:
+                del t
+
+
 def profile_kernel(args, wl):
     """One kernel alone, args.steps times, for counter collection."""
     import torch
@@ -545,6 +602,8 @@ def main():
                          "(CPU only) and print the policies' SLO attainment and latency")
     ap.add_argument("--sim-oracle", action="store_true", help="with --simulate: also time the simulator oracle")
     ap.add_argument("--load", type=float, default=0.8, help="with --simulate: offered load (fraction of capacity)")
+    ap.add_argument("--migrate", action="store_true",
+                    help="time the latent's migration between sequence-parallel layouts (plan + one-GPU execution)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -574,6 +633,9 @@ def main():
         return
     if args.cost_table:
         run_cost_table(args)
+        return
+    if args.migrate:
+        run_migrate(args)
         return
     wl = synth.get_workload(args.workload)
     if args.profile_kernel:
