@@ -150,6 +150,8 @@ for _mw in [
                          linear_std=0.02 * (5120 / 256) ** 0.5),
                   2, 16, (1, 2, 2),
                   "small bf16 step: 2 blocks, D 256, 16 latent channels, patch 1x2x2, requests of 72 and 60 tokens"),
+    ModelWorkload("step_image_1024", WORKLOADS["image_1024"], 60, 16, (1, 2, 2),
+                  "1024x1024 image step: 60 blocks of the image block, latent 16x128x128, patch 1x2x2"),
     ModelWorkload("step_video_480p", WORKLOADS["video_480p"], 40, 16, (1, 2, 2),
                   "480p video step: 40 blocks of the 480p block, latent 16x21x60x104, patch 1x2x2"),
     ModelWorkload("step_video_720p", WORKLOADS["video_720p"], 40, 16, (1, 2, 2),
