@@ -365,11 +365,23 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   return DIT_OK;
 }
 
+// The bf16 attention numbers its work items (256-query tiles x heads) in int
+// and splits them over the XCDs with products that must stay below 2^31.
+dit_status check_attn_items(const int32_t* cu, int n_req, int n_heads) {
+  int64_t items = 0;
+  for (int r = 0; r < n_req; ++r) items += (int64_t)(cu[r + 1] - cu[r] + 255) / 256 * n_heads;
+  if (items > (1 << 27))
+    return fail(DIT_ERR_UNSUPPORTED, "attention of %lld work items (at most 2^27 query tiles x heads)",
+                (long long)items);
+  return DIT_OK;
+}
+
 dit_status check_block_call(const dit_block_config* c, const dit_block_weights* w, const dit_varlen* vl, bool pre,
                             bool post) {
   DIT_TRY(check_cfg(c));
   DIT_TRY(check_weights(c, w, pre, post));
   DIT_TRY(check_varlen(vl, post));
+  DIT_TRY(check_attn_items(vl->cu_seqlens, vl->n_req, c->n_heads));
   if (pre) {
     RopeTable tab;
     DIT_TRY(check_rope_table(vl, c->rope_sections, &tab));
@@ -615,6 +627,7 @@ dit_status dit_attention_varlen(const void* q, const void* k, const void* v, voi
     if (strides[i] < width || strides[i] % vec)
       return fail(DIT_ERR_INVALID_ARG, "row stride %lld: must be >= n_heads*head_dim = %lld and a multiple of %lld",
                   (long long)strides[i], (long long)width, (long long)vec);
+  DIT_TRY(check_attn_items(cu_q, n_req, n_heads));
   return run_attention(q, k, v, o, q_row_stride, k_row_stride, v_row_stride, o_row_stride, make_req(cu_q, n_req),
                        make_req(cu_k, n_req), n_heads, head_dim, softmax_scale, dtype, stream);
 }
@@ -774,6 +787,7 @@ dit_status dit_denoise_step(const dit_model_config* cfg, const dit_model_weights
   const dit_block_config* c = &cfg->block;
   RopeTable rope;
   DIT_TRY(check_rope_table(vl, c->rope_sections, &rope));
+  DIT_TRY(check_attn_items(vl->cu_seqlens, vl->n_req, c->n_heads));
   DIT_TRY(check_ptr(latent, "latent")); DIT_TRY(check_ptr(t, "t")); DIT_TRY(check_ptr(dt, "dt"));
   DIT_TRY(check_ptr(kv, "kv")); DIT_TRY(check_ptr(latent_out, "latent_out"));
   const size_t need = model_layout(cfg, vl, nullptr, nullptr);

@@ -249,3 +249,13 @@ def test_text_kv_and_latent_stages_reject_bad_arguments():
     assert L.dit_unpatchify_euler(ctypes.byref(cfg.c), ctypes.byref(vl.c), P, P, None, P, S) == \
         B.DIT_ERR_INVALID_ARG
     assert L.dit_patchify(ctypes.byref(cfg.c), ctypes.byref(vl.c), P_MIS, P, S) == B.DIT_ERR_INVALID_ARG
+
+
+def test_attention_rejects_too_many_work_items():
+    """2^30 query rows x 64 heads is more 256-row work items than the kernel
+    numbers (2^27): rejected on the host, nothing launched."""
+    L = _lib()
+    cu, pcu = _cu([0, 1 << 30])
+    st = L.dit_attention_varlen(P, P, P, P, 64 * 128, 64 * 128, 64 * 128, 64 * 128, pcu, pcu, 1, 64, 128, 0.1,
+                                B.DIT_BF16, ctypes.c_void_p(0))
+    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error()
