@@ -184,3 +184,26 @@ def test_step_fullsize_properties(name):
     ref = M.patchify_packed(O.decode(s.model["latent"]), mw.in_channels, list(mw.block.grids), mw.patch)
     got = tok.view(torch.int16).cpu().numpy().view(np.uint16)
     assert np.array_equal(got, synth.bf16_bits(ref.astype(np.float32))), "720p patchify bits"
+
+
+def test_step_graph_capture():
+    """The step launches no memset, allocates nothing and never synchronises,
+    so it can be captured in a HIP graph: three replays (with eager steps in
+    between) each equal the eager result bit for bit."""
+    mw = synth.get_model_workload("step_small_bf16")
+    s = DeviceStep(mw)
+    ref = s.step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    out = torch.empty_like(ref)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        s.B.denoise_step(s.cfg, s.w, s.vl, s.dm["latent"], s.dm["t"], s.dm["dt"], s.kv, out, s.ws, stream=stream)
+    for rep in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"replay {rep} differs"
+        s.step()
+        torch.cuda.synchronize()
