@@ -246,15 +246,16 @@ def model_tensor_specs(mw: ModelWorkload) -> Dict[str, TensorSpec]:
     return {s.name: s for s in specs}
 
 
-def generate_model_inputs(mw: ModelWorkload, threads: Optional[int] = None):
+def generate_model_inputs(mw: ModelWorkload, threads: Optional[int] = None, n_blocks: Optional[int] = None):
     """(model tensors, [block weight dicts]).  Block b's weights use the block
     recipe with tensor ids offset by 1000 * (b + 1); they omit the blocks' own
-    timestep MLP, which the step does not read."""
+    timestep MLP, which the step does not read.  n_blocks: only the first
+    n_blocks blocks (their values do not depend on how many are drawn)."""
     specs = model_tensor_specs(mw)
     model = {n: generate_tensor(s, mw.block, threads) for n, s in specs.items()}
     bspecs = block_tensor_specs(mw.block)
     blocks = []
-    for b in range(mw.n_blocks):
+    for b in range(mw.n_blocks if n_blocks is None else n_blocks):
         d = {}
         for n in WEIGHT_NAMES:
             if n in ("w_t1", "b_t1", "w_t2", "b_t2"):

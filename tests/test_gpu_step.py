@@ -3,6 +3,8 @@ dit_unpatchify_euler) against the step oracle, plus its invariants at the
 720p video size.  Tolerances: fp32 max |g - r| <= 1e-4; bf16 cosine >= 0.9999
 and max relative error <= 2e-2, on the next latent and on its update
 latent_out - latent (where all of the model's signal is)."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -23,7 +25,7 @@ class DeviceStep:
         self.B, self.mw = B, mw
         wl = mw.block
         self.n_blocks = n_blocks or mw.n_blocks
-        self.model, self.blocks = inputs if inputs is not None else synth.generate_model_inputs(mw)
+        self.model, self.blocks = inputs if inputs is not None else synth.generate_model_inputs(mw, n_blocks=n_blocks)
         self.blocks = self.blocks[:self.n_blocks]
         self.dm = {k: dev(v) for k, v in self.model.items()}
         self.db = [{k: dev(v) for k, v in b.items()} for b in self.blocks]
@@ -207,3 +209,24 @@ def test_step_graph_capture():
         assert torch.equal(out, ref), f"replay {rep} differs"
         s.step()
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name", ["step_video_480p", "step_video_720p"])
+def test_step_fullsize_vs_golden(name):
+    """A whole-size step cut to its first block (the per-block work of the
+    40-block step): the update latent_out - latent of a seeded sample of
+    tokens against the oracle's velocity times dt, from
+    tests/golden/make_step_golden.py (oracle only)."""
+    mw = synth.get_model_workload(name)
+    gold = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", f"{name}_1block.npz"))
+    rows, v = gold["rows"], gold["v"].astype(np.float64)
+    log(f"[step] {name} with 1 block vs golden: {len(rows)} tokens")
+    s = DeviceStep(mw, n_blocks=1)
+    out = s.step().cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    grids, C, patch = list(mw.block.grids), mw.in_channels, mw.patch
+    lat = O.decode(s.model["latent"])
+    upd = (M.patchify_packed(out, C, grids, patch) - M.patchify_packed(lat, C, grids, patch))[rows]
+    cu = np.asarray(mw.block.cu_seqlens())
+    dts = O.decode(s.model["dt"])[np.searchsorted(cu, rows, side="right") - 1]
+    check(upd, dts[:, None] * v, "bf16", f"{name} 1-block update on sampled tokens")
