@@ -46,7 +46,7 @@ extern "C" {
 #endif
 
 #define DIT_MAX_REQ 64
-#define DIT_ABI_VERSION 1
+#define DIT_ABI_VERSION 2
 
 typedef enum {
   DIT_OK = 0,
@@ -113,13 +113,17 @@ typedef struct {
 size_t dit_block_workspace_size(const dit_block_config *cfg, const dit_varlen *vl);
 
 /* One block: y = Block(x; t, txt).  x, y: [rows, D]; t: device fp32 [n_req]
- * timesteps; txt: [txt_rows, D] text embeddings.  y may equal x.  The
- * workspace (ws, ws_bytes) must hold dit_block_workspace_size bytes, 256-byte
- * aligned; its contents are scratch. */
+ * timesteps; mod: device fp32 [n_req, 6, D] modulation vectors in the order
+ * of dit_timestep_modulation, or NULL to compute them from t (with mod given,
+ * t may be NULL and the block's w_t1..b_ada are not read: a model whose
+ * blocks share one timestep MLP passes each block's modulation here);
+ * txt: [txt_rows, D] text embeddings.  y may equal x.  The workspace (ws,
+ * ws_bytes) must hold dit_block_workspace_size bytes, 256-byte aligned; its
+ * contents are scratch. */
 dit_status dit_block_forward(const dit_block_config *cfg, const dit_block_weights *w,
                              const dit_varlen *vl, const void *x, const float *t,
-                             const void *txt, void *y, void *ws, size_t ws_bytes,
-                             hipStream_t stream);
+                             const float *mod, const void *txt, void *y, void *ws,
+                             size_t ws_bytes, hipStream_t stream);
 
 /* Steps before self-attention, on this GPU's rows: conditioning mod = adaLN(t)
  * (device fp32 [n_req, 6, D], written), modulated LayerNorm, QKV projection,

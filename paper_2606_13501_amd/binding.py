@@ -132,7 +132,7 @@ def lib() -> ctypes.CDLL:
     PM, PMW = ctypes.POINTER(CModelConfig), ctypes.POINTER(CModelWeights)
     sig = {
         "dit_block_workspace_size": (sz, [PC, PV]),
-        "dit_block_forward": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_block_forward": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_block_pre_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
         "dit_block_post_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_timestep_modulation": (i32, [PC, PW, i32, vp, vp, vp, sz, vp]),
@@ -258,9 +258,10 @@ def block_workspace_size(cfg: BlockConfig, vl: Varlen) -> int:
     return int(lib().dit_block_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c)))
 
 
-def block_forward(cfg, weights: CWeights, vl, x, t, txt, y, ws, stream=None):
+def block_forward(cfg, weights: CWeights, vl, x, t, txt, y, ws, stream=None, mod=None):
+    """mod: optional precomputed modulation [n_req, 6, D] fp32 (t may then be None)."""
     _check(lib().dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
-                                   _ptr(t), _ptr(txt), _ptr(y), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _ptr(t), _ptr(mod), _ptr(txt), _ptr(y), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream(stream)), "dit_block_forward")
 
 

@@ -156,15 +156,17 @@ dit_status check_cfg(const dit_block_config* c) {
 // tmlp: the block's own timestep MLP is read (not by the denoising step, whose
 // blocks share the model's).
 dit_status check_weights(const dit_block_config* c, const dit_block_weights* w, bool pre, bool post,
-                         bool tmlp = true) {
+                         bool tmlp = true, bool ada = true) {
   if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
   const bool qn = c->qk_norm != 0;
   if (pre && tmlp) {
     DIT_TRY(check_ptr(w->w_t1, "w_t1")); DIT_TRY(check_ptr(w->b_t1, "b_t1"));
     DIT_TRY(check_ptr(w->w_t2, "w_t2")); DIT_TRY(check_ptr(w->b_t2, "b_t2"));
   }
-  if (pre) {
+  if (pre && ada) {
     DIT_TRY(check_ptr(w->w_ada, "w_ada")); DIT_TRY(check_ptr(w->b_ada, "b_ada"));
+  }
+  if (pre) {
     DIT_TRY(check_ptr(w->w_qkv, "w_qkv")); DIT_TRY(check_ptr(w->b_qkv, "b_qkv"));
     DIT_TRY(check_ptr(w->g_q, "g_q", !qn)); DIT_TRY(check_ptr(w->g_k, "g_k", !qn));
   }
@@ -377,9 +379,9 @@ dit_status check_attn_items(const int32_t* cu, int n_req, int n_heads) {
 }
 
 dit_status check_block_call(const dit_block_config* c, const dit_block_weights* w, const dit_varlen* vl, bool pre,
-                            bool post) {
+                            bool post, bool cond = true) {
   DIT_TRY(check_cfg(c));
-  DIT_TRY(check_weights(c, w, pre, post));
+  DIT_TRY(check_weights(c, w, pre, post, cond, cond));
   DIT_TRY(check_varlen(vl, post));
   DIT_TRY(check_attn_items(vl->cu_seqlens, vl->n_req, c->n_heads));
   if (pre) {
@@ -533,12 +535,13 @@ size_t dit_block_workspace_size(const dit_block_config* cfg, const dit_varlen* v
 }
 
 dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weights* w, const dit_varlen* vl,
-                             const void* x, const float* t, const void* txt, void* y, void* ws, size_t ws_bytes,
-                             hipStream_t stream) {
+                             const void* x, const float* t, const float* mod, const void* txt, void* y, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
   g_last_error.clear();
-  DIT_TRY(check_block_call(cfg, w, vl, true, true));
+  DIT_TRY(check_block_call(cfg, w, vl, true, true, mod == nullptr));
   DIT_TRY(check_ptr(x, "x"));
-  DIT_TRY(check_ptr(t, "t"));
+  if (mod) DIT_TRY(check_ptr(mod, "mod"));
+  else DIT_TRY(check_ptr(t, "t"));
   DIT_TRY(check_ptr(txt, "txt"));
   DIT_TRY(check_ptr(y, "y"));
   Workspace W;
@@ -546,11 +549,15 @@ dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weight
   const int D = cfg->hidden;
   const size_t es = elem_size(cfg->dtype);
   const ReqTable req = make_req(vl->cu_seqlens, vl->n_req);
-  DIT_TRY(run_cond(cfg, w, vl->n_req, t, W.mod, W.e, W.a1, W.c, stream));
-  DIT_TRY(pre_attention_impl(cfg, w, vl, x, W.mod, W.qkv, W, stream));
+  const float* m = mod;
+  if (!m) {
+    DIT_TRY(run_cond(cfg, w, vl->n_req, t, W.mod, W.e, W.a1, W.c, stream));
+    m = W.mod;
+  }
+  DIT_TRY(pre_attention_impl(cfg, w, vl, x, m, W.qkv, W, stream));
   DIT_TRY(run_attention(W.qkv, W.qkv + D * es, W.qkv + 2 * D * es, W.o, 3 * D, 3 * D, 3 * D, D, req, req,
                         cfg->n_heads, cfg->head_dim, 1.0f / sqrtf((float)cfg->head_dim), cfg->dtype, stream));
-  return post_attention_impl(cfg, w, vl, x, W.o, txt, W.mod, y, W, stream);
+  return post_attention_impl(cfg, w, vl, x, W.o, txt, m, y, W, stream);
 }
 
 dit_status dit_block_pre_attention(const dit_block_config* cfg, const dit_block_weights* w, const dit_varlen* vl,

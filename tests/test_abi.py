@@ -43,7 +43,7 @@ def test_library_exports_every_header_function():
 
 def test_abi_version_and_strings():
     L = _lib()
-    assert L.dit_abi_version() == 1
+    assert L.dit_abi_version() == 2
     assert L.dit_status_string(B.DIT_ERR_WORKSPACE) == b"workspace too small"
     assert L.dit_status_string(B.DIT_OK) == b"ok"
 
@@ -136,28 +136,37 @@ def test_block_validation_and_workspace():
     need = L.dit_block_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c))
     assert need > 0 and need % 256 == 0
     # workspace too small, misaligned, missing
-    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P,
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, None, P, P,
                             ctypes.c_void_p(0x100000), need - 256, S)
     assert r == B.DIT_ERR_WORKSPACE
-    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P,
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, None, P, P,
                             ctypes.c_void_p(0x100010), need, S)
     assert r == B.DIT_ERR_WORKSPACE
     # a weight missing
     w.w_up = None
-    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P, P, need, S)
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, None, P, P, P, need, S)
     assert r == B.DIT_ERR_INVALID_ARG and b"w_up" in L.dit_last_error()
+    # with a precomputed modulation the block's timestep MLP and adaLN weights are not needed
+    w.w_up = P.value
+    w.w_t1 = w.w_ada = None
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, None, P, P, P, need, S)
+    assert r == B.DIT_ERR_INVALID_ARG and b"w_t1" in L.dit_last_error()
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, None, P, P, P, None, need, S)
+    assert r == B.DIT_ERR_WORKSPACE, L.dit_last_error()
+    w.w_up = None
     # bad configs
     for kw, code in [(dict(head_dim=64, heads=4, sections=(0, 32, 32)), B.DIT_ERR_UNSUPPORTED),
                      (dict(sections=(0, 64, 62)), B.DIT_ERR_INVALID_ARG),
                      (dict(hidden=250), B.DIT_ERR_INVALID_ARG)]:
         cfg2, w2, vl2 = _block_structs(**kw)
-        r = L.dit_block_forward(ctypes.byref(cfg2.c), ctypes.byref(w2), ctypes.byref(vl2.c), P, P, P, P, P, 1 << 40, S)
+        r = L.dit_block_forward(ctypes.byref(cfg2.c), ctypes.byref(w2), ctypes.byref(vl2.c), P, P, None, P, P, P, 1 << 40,
+                                S)
         assert r == code, (kw, r, L.dit_last_error())
         assert L.dit_block_workspace_size(ctypes.byref(cfg2.c), ctypes.byref(vl2.c)) == 0
     # rows of a request that do not fit its grid
     cfg, w, vl = _block_structs()
     vl = B.Varlen([0, 17, 40], [0, 8, 20], [(1, 4, 4), (1, 4, 6)])
-    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, P, P, P, 1 << 40, S)
+    r = L.dit_block_forward(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, P, None, P, P, P, 1 << 40, S)
     assert r == B.DIT_ERR_INVALID_ARG and b"exceed its grid" in L.dit_last_error()
 
 

@@ -130,3 +130,22 @@ def test_shard_rows_equal_full_rows():
     B.block_pre_attention(db.cfg, db.w, vls, xs, db.d["t"], mod, shard, ws)
     torch.cuda.synchronize()
     assert torch.equal(shard, full[a:b])
+
+
+def test_block_forward_with_precomputed_modulation():
+    """dit_block_forward with mod given (t NULL, the block's timestep MLP and
+    adaLN weights absent) equals the call that computes mod from t, bit for bit."""
+    wl = synth.get_workload("image_1024")
+    db = DeviceBlock(wl)
+    B = db.B
+    y_ref = db.forward()
+    D = wl.hidden
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    B.timestep_modulation(db.cfg, db.w, db.d["t"], mod, db.ws)
+    d2 = dict(db.d)
+    for n in ("w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada"):
+        d2[n] = None
+    y = torch.empty_like(y_ref)
+    B.block_forward(db.cfg, B.make_weights(d2), db.vl, db.d["x"], None, db.d["txt"], y, db.ws, mod=mod)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_ref)
