@@ -3,9 +3,11 @@ tokens) and the packed sequence-parallel share (four requests, 5 attention
 heads over 121,672 rows), in the launch configuration the benchmark times.
 
 The GPU computes every row; the oracle computes a seeded sample of rows
-(first and last row of every request, frame boundaries, random rows) from the
-same inputs.  Self-attention stages use seeded q, k, v; the whole block is
-compared with expected rows written by tests/golden/make_block_golden.py."""
+(first and last row of every request, frame boundaries, random rows: 2048
+per request for self-attention, 256 for the per-row stages around it) from
+the same inputs.  Self-attention stages use seeded q, k, v; the whole block is
+compared with expected rows written by tests/golden/make_block_golden.py.
+The memory-bound stages are compared on every row."""
 import os
 
 import numpy as np
@@ -40,7 +42,7 @@ def test_self_attention_full_size(name):
     cu = wl.cu_attn()
     B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], o, cu, cu, H, d)
     torch.cuda.synchronize()
-    rows = synth.generate_sampled_rows(wl, 24, sample_id=3, attn=True)
+    rows = synth.generate_sampled_rows(wl, 2048, sample_id=3, attn=True)
     g = host(o[torch.from_numpy(rows).cuda()])
     del t, o
     ref = O.attention_varlen(O.decode(qkv[:, :W]), O.decode(qkv[:, W:2 * W]), O.decode(qkv[:, 2 * W:]), cu, cu, H, d,
@@ -62,7 +64,7 @@ def test_pre_post_attention_full_size(name):
     y = empty((T, D), "bf16")
     B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], dev(o_in), db.d["txt"], mod, y, db.ws)
     torch.cuda.synchronize()
-    rows = synth.generate_sampled_rows(wl, 24, sample_id=4)
+    rows = synth.generate_sampled_rows(wl, 256, sample_id=4)
     idx = torch.from_numpy(rows).cuda()
     g_qkv = host(qkv[idx])
     g_y = host(y[idx])
@@ -97,3 +99,53 @@ def test_block_full_size_vs_golden(name):
     x = O.decode(db.inp["x"][rows])
     check(g, ref, "bf16", f"{name} block y ({len(rows)} sampled rows)")
     check(g - x, ref - x, "bf16", f"{name} block y - x")
+
+
+def test_memory_bound_stages_all_rows():
+    """The 720p block's memory-bound stages on all 75,600 rows, each on its
+    own inputs: modulated LayerNorm (S1, S10) with the GPU's own modulation,
+    affine LayerNorm (S6), per-head RMSNorm + 3D rotary on seeded q and k (S3),
+    and the standalone gated residual."""
+    wl = synth.get_workload("video_720p")
+    log(f"case all-row memory-bound stages {wl.name}: rows {wl.n_rows}")
+    db = DeviceBlock(wl, names=["x", "t", "txt", "w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada", "g_q", "g_k",
+                                "g_ca", "b_ca", "b_o"])
+    B = db.B
+    T, D, H, d = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
+    cu = wl.cu_seqlens()
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    B.timestep_modulation(db.cfg, db.w, db.d["t"], mod, db.ws)
+    out = empty((T, D), "bf16")
+    B.adaln_modulate(db.d["x"], mod[:, 0], mod[:, 1], 6 * D, cu, wl.ln_eps, out)
+    torch.cuda.synchronize()
+    x = O.decode(db.inp["x"])
+    m = host(mod)
+    ref = O.modulate(O.layer_norm(x, wl.ln_eps), m[0, 0], m[0, 1])
+    check(host(out), ref, "bf16", "modulated LayerNorm, all rows")
+    del ref
+    B.layer_norm_affine(db.d["x"], db.d["g_ca"], db.d["b_ca"], wl.ln_eps, out)
+    torch.cuda.synchronize()
+    ref = O.layer_norm(x, wl.ln_eps) * O.decode(db.inp["g_ca"]) + O.decode(db.inp["b_ca"])
+    check(host(out), ref, "bf16", "affine LayerNorm, all rows")
+    del ref
+    z_bits = synth.draw((T, D), (31, 1))
+    gate = mod[:, 2]
+    B.gated_residual(db.d["x"], dev(z_bits), db.d["b_o"], gate, 6 * D, cu, out)
+    torch.cuda.synchronize()
+    ref = x + m[0, 2] * (O.decode(z_bits) + O.decode(db.inp["b_o"]))
+    check(host(out), ref, "bf16", "gated residual, all rows")
+    del ref, out, z_bits
+    qk_bits = synth.draw((T, 2 * D), (31, 2))
+    qk = dev(qk_bits)
+    vl = B.Varlen(cu, wl.cu_txt(), list(wl.grids))
+    B.qk_norm_rope(qk[:, :D], qk[:, D:], H, d, db.d["g_q"], db.d["g_k"], wl.rms_eps, wl.rope_sections,
+                   wl.rope_theta, vl)
+    torch.cuda.synchronize()
+    g = host(qk)
+    del qk
+    cfg, ovl = O.config_from_workload(wl), O.varlen_from_workload(wl)
+    u = O.decode(qk_bits)
+    for part, gain in ((slice(0, D), "g_q"), (slice(D, 2 * D), "g_k")):
+        ref = O.rope_for_rows(O.rms_norm_heads(u[:, part], O.decode(db.inp[gain]), H, d, wl.rms_eps), cfg, ovl)
+        check(g[:, part], ref, "bf16", f"RMSNorm + rotary ({gain[-1]}), all rows")
+        del ref
