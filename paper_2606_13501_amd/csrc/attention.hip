@@ -22,9 +22,12 @@
 // The loop is software-pipelined in half steps of one query block (32 rows):
 // while the matrix core computes S of the next tile for one block and the PV
 // product of the current tile, the vector ALU runs the softmax of the other
-// block's finished scores.  Softmax is fp32 with exp2 and log2(e) folded into
-// the scale, against a per-row reference fixed for the whole pass (the first
-// tile's row max): no rescale of O inside the loop.  The pass also tracks the
+// block's finished scores.  Softmax is fp32 with exp2, against a per-row
+// reference fixed for the whole pass (the first tile's row max): no rescale of
+// O inside the loop.  Q is scaled by log2(e)/sqrt(d) once, in registers, and
+// the first S MFMA of a tile accumulates onto the negated reference, so the
+// matrix core delivers score - reference in log2 units and the softmax is an
+// exp2, a conversion and an add per score.  The pass also tracks the
 // true row max; if any row of the workgroup exceeded its reference by more
 // than 2^64 (where the probabilities could overflow), the work item is
 // recomputed with the exact max as reference, so the result is always the
@@ -109,6 +112,11 @@ __device__ __forceinline__ void mfma_s_first(f32x16& d, const bf16x8& a, const b
   // same registers from tile to tile, without copies
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "+v"(d) : "v"(a), "v"(b));
 }
+// the first MFMA of a score block starting from the bias c (the negated row
+// references) instead of zero
+__device__ __forceinline__ void mfma_s_bias(f32x16& d, const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "+v"(d) : "v"(a), "v"(b), "v"(c));
+}
 __device__ __forceinline__ void mfma_s_acc(f32x16& d, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "v"(b));
 }
@@ -170,6 +178,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // the Q loads complete here, before any tile load is issued (otherwise the
   // compiler's wait for them would also wait for the tile loads, in the loop)
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  // scores in log2 units straight from the matrix core: q * log2(e)/sqrt(d),
+  // rounded to bf16 once (a relative error of at most 2^-9 per element, the
+  // size of q's own rounding)
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc) {
+      typedef float f32x8 __attribute__((ext_vector_type(8)));
+      const f32x8 f = __builtin_convertvector(qf[qb][kc], f32x8) * scale_log2;
+      qf[qb][kc] = __builtin_convertvector(f, bf16x8);
+    }
 
   // ---- global -> LDS.  A tile (K or V) is 8 pieces of 1 KiB = 4 key rows of
   // 256 B; wave w loads pieces 2 w, 2 w + 1 of both.  Lane i of piece p
@@ -232,6 +251,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // that pass also tracks x_max = max(score - m_ref), so a row whose sum had
   // overflowed gets m_ref = its exact max in a last pass.
   float m_ref[2], x_max[2];
+  f32x16 nref[2];       // nref[qb]: -m_ref[qb] in every element, the bias of S
   float l_run[2][2];    // this lane's share of the row sums, two partial sums per block
 
   // keys past the request end (ragged last tile) score -inf
@@ -246,8 +266,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   typedef float f32x2 __attribute__((ext_vector_type(2)));
   auto soft_pair = [&](int qb, int j, auto track) __attribute__((always_inline)) {
     const int kc = j >> 2, e = 2 * (j & 3);
-    const float x0 = fmaf(sq[qb][2 * j], scale_log2, -m_ref[qb]);
-    const float x1 = fmaf(sq[qb][2 * j + 1], scale_log2, -m_ref[qb]);
+    const float x0 = sq[qb][2 * j], x1 = sq[qb][2 * j + 1];   // score - m_ref, log2 units
     if (decltype(track)::value) x_max[qb] = fmaxf(fmaxf(x_max[qb], x0), x1);
     const float p0 = __builtin_amdgcn_exp2f(x0), p1 = __builtin_amdgcn_exp2f(x1);
     const bf16x2 pr = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
@@ -321,7 +340,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
         if (i + 1 < 8) vf[i + 1] = v_frag(so_v, i + 1);
       }
       if (WS) {
-        if (i == 0) mfma_s_first(sq[h], kf[i], qf[h][i]);
+        if (i == 0) mfma_s_bias(sq[h], kf[i], qf[h][i], nref[h]);
         else mfma_s_acc(sq[h], kf[i], qf[h][i]);
       }
       oacc[i & 3][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pq[h][i >> 2], oacc[i & 3][h], 0, 0, 0);
@@ -398,9 +417,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
 #pragma unroll
           for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sq[qb][v]);
           auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          m_ref[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+          m_ref[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         }
       }
+      // S(0) was computed from zero: subtract the reference here; the later
+      // tiles start from it
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          sq[qb][v] -= m_ref[qb];
+          nref[qb][v] = -m_ref[qb];
+        }
 #pragma unroll
       for (int j = 0; j < 8; ++j) soft_pair(0, j, track);   // P(0) block 0
     }
