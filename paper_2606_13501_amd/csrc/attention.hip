@@ -1,37 +1,35 @@
 // Scaled dot-product attention over a packed batch, non-causal (the denoising
 // step attends bidirectionally over the whole latent sequence).
 //
-// bf16, head_dim 128: flash-style kernel for gfx950.  One 256-thread
-// workgroup (4 waves, one per SIMD) owns 256 query rows of one (request,
-// head); each wave owns 64 of them, so every K/V byte read from LDS feeds 64
-// queries.  K and V tiles of 32 keys stream from global memory straight into
-// an LDS ring of 4 tiles (buffer loads with the lds modifier: no registers,
-// no LDS store instructions), issued 3 tiles ahead of use; a deeper ring lets
-// the workgroups streaming one head drift further apart and costs L2 hits.
-// Both are stored row-major with their 16-byte chunks XOR-swizzled per row.
+// bf16, head_dim 128: flash-style kernel for gfx950.  One 512-thread
+// workgroup (8 waves, two per SIMD) owns 256 query rows of one (request,
+// head); each wave owns 32 of them.  Two waves per SIMD let the matrix core
+// run one wave's MFMAs while the other wave's softmax, LDS reads and waits
+// are in progress, with no hand-made phase offset between them.  K and V
+// tiles of 64 keys stream from global memory straight into an LDS ring of 4
+// tiles (buffer loads with the lds modifier: no registers, no LDS store
+// instructions), issued 3 tiles ahead of use.  Both are stored row-major with
+// their 16-byte chunks XOR-swizzled per row.
 //
 // Per tile a wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K as
-// the A operand, Q fragments held in registers), so every lane holds the
-// scores of its query rows: P^T feeds the PV MFMA straight from the lane's
-// registers, and O^T = V^T P^T leaves the output of the same rows in the same
-// lane.  The V^T operand is read from the row-major V tile with the
-// transposing LDS read (ds_read_b64_tr_b16); its source rows are chosen so
-// that the 8 keys a lane contributes match the order of the lane's scores
-// (bits 2 and 3 of the key index swapped).
+// the A operand, Q fragments held in registers), two 32-key halves as two
+// independent accumulation chains, so every lane holds the scores of its
+// query row: P^T feeds the PV MFMA straight from the lane's registers, and
+// O^T = V^T P^T leaves the output of the same row in the same lane.  The V^T
+// operand is read from the row-major V tile with the transposing LDS read
+// (ds_read_b64_tr_b16); its source rows are chosen so that the 8 keys a lane
+// contributes match the order of the lane's scores (bits 2 and 3 of the key
+// index swapped).
 //
-// The loop is software-pipelined in half steps of one query block (32 rows):
-// while the matrix core computes S of the next tile for one block and the PV
-// product of the current tile, the vector ALU runs the softmax of the other
-// block's finished scores.  Softmax is fp32 with exp2, against a per-row
-// reference fixed for the whole pass (the first tile's row max): no rescale of
-// O inside the loop.  Q is scaled by log2(e)/sqrt(d) once, in registers, and
-// the first S MFMA of a tile accumulates onto the negated reference, so the
-// matrix core delivers score - reference in log2 units and the softmax is an
-// exp2, a conversion and an add per score.  The pass also tracks the
-// true row max; if any row of the workgroup exceeded its reference by more
-// than 2^64 (where the probabilities could overflow), the work item is
-// recomputed with the exact max as reference, so the result is always the
-// exact softmax up to rounding.
+// Softmax is fp32 with exp2, against a per-row reference fixed for the whole
+// pass (the first tile's row max): no rescale of O inside the loop.  Q is
+// scaled by log2(e)/sqrt(d) once, in registers, and the first S MFMA of a
+// tile accumulates onto the negated reference, so the matrix core delivers
+// score - reference in log2 units and the softmax is an exp2, a conversion
+// and an add per score.  If any row of the workgroup exceeded its reference
+// by more than 2^64 (where the probabilities could overflow), the work item
+// is recomputed with a safe reference, so the result is always the exact
+// softmax up to rounding.
 //
 // fp32: one thread per (query row, head) with an exact online softmax.
 #include <float.h>
@@ -46,11 +44,11 @@ namespace {
 
 constexpr int D = 128;                 // head_dim of the bf16 kernel
 constexpr int BQ = 256;                // query rows per workgroup
-constexpr int BKV = 32;                // keys per tile
-constexpr int kWaves = 4;
+constexpr int BKV = 64;                // keys per tile
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kRing = 4;               // LDS ring of K/V tiles
-constexpr int kTileBytes = BKV * D * 2;          // one K or V tile (8 KiB)
+constexpr int kTileBytes = BKV * D * 2;          // one K or V tile (16 KiB)
 constexpr int kSlotBytes = 2 * kTileBytes;       // K tile + V tile
 constexpr int kPieces = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave and operand (2)
 constexpr int kLoadsPerTile = 2 * kPieces;       // this wave's loads of one tile
@@ -88,32 +86,19 @@ __device__ __forceinline__ void load_lds16(const u32x4& desc, uint32_t voff, uin
 #pragma clang diagnostic pop
 template <int N> __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N)); }
 
-// wait until at most `tiles` of this wave's most recently issued tiles are pending
-__device__ __forceinline__ void wait_tiles(int tiles) {
-  if (tiles <= 0) wait_vmcnt<0>();
-  else if (tiles == 1) wait_vmcnt<1 * kLoadsPerTile>();
-  else if (tiles == 2) wait_vmcnt<2 * kLoadsPerTile>();
-  else if (tiles == 3) wait_vmcnt<3 * kLoadsPerTile>();
-  else if (tiles == 4) wait_vmcnt<4 * kLoadsPerTile>();
-  else if (tiles == 5) wait_vmcnt<5 * kLoadsPerTile>();
-  else if (tiles == 6) wait_vmcnt<6 * kLoadsPerTile>();
-  else wait_vmcnt<7 * kLoadsPerTile>();
-}
-
-// S^T MFMAs of the main loop as inline assembly with vector-register
-// operands: the compiler would otherwise place the scores in accumulation
-// registers and copy them to vector registers for the softmax.  It does not
-// see these as MFMAs, so the distance from the last MFMA of a score block to
-// its first vector read is kept by hand: score_guard (at least 19 wait
-// states) takes the block as an in-out operand, so no read of it can be
-// scheduled before the guard.
+// S^T MFMAs as inline assembly with vector-register operands: the compiler
+// would otherwise place the scores in accumulation registers and copy them to
+// vector registers for the softmax.  It does not see these as MFMAs, so the
+// distance from the last MFMA of a score block to its first vector read is
+// kept by hand: score_guard (at least 19 wait states) takes the block as an
+// in-out operand, so no read of it can be scheduled before the guard.
 __device__ __forceinline__ void mfma_s_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
   // d as an in-out operand (its old value unused) keeps the scores in the
   // same registers from tile to tile, without copies
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "+v"(d) : "v"(a), "v"(b));
 }
 // the first MFMA of a score block starting from the bias c (the negated row
-// references) instead of zero
+// reference) instead of zero
 __device__ __forceinline__ void mfma_s_bias(f32x16& d, const bf16x8& a, const bf16x8& b, const f32x16& c) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "+v"(d) : "v"(a), "v"(b), "v"(c));
 }
@@ -129,8 +114,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
     float scale_log2, AttnWork work) {
-  // slot t % kRing holds K(t) (first 8 KiB) and V(t)
+  // slot t % kRing holds K(t) (first 16 KiB) and V(t)
   __shared__ __attribute__((aligned(1024))) char smem[kRing * kSlotBytes];
+  __shared__ int redo_flag[2];   // one flag per pass that may ask for another
 
   // ---- work item.  Workgroups are dispatched to the XCDs round-robin, so
   // workgroup b runs on XCD b % 8 as that XCD's (b / 8)-th.  Each XCD takes
@@ -162,36 +148,30 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
   const int fr = lane & 31;
   const int fh = lane >> 5;
+  if (tid < 2) redo_flag[tid] = 0;
 
-  // ---- Q fragments (B operand of S^T): query q0 + 64 wave + 32 qb + fr,
-  // d 16 kc + 8 fh .. +7
-  bf16x8 qf[2][8];
-  int my_q[2];
+  // ---- Q fragments (B operand of S^T): query q0 + 32 wave + fr, d 16 kc +
+  // 8 fh .. +7, scaled by log2(e)/sqrt(d) and rounded to bf16 once (a
+  // relative error of at most 2^-9 per element, the size of q's own rounding)
+  const int my_q = q0 + 32 * wave + fr;
+  bf16x8 qf[8];
+  {
+    const bf16* qp = Q + (int64_t)min(my_q, q_end - 1) * qs + head * D + 8 * fh;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    my_q[qb] = q0 + 64 * wave + 32 * qb + fr;
-    const int qrow = min(my_q[qb], q_end - 1);
-    const bf16* qp = Q + (int64_t)qrow * qs + head * D + 8 * fh;
-#pragma unroll
-    for (int kc = 0; kc < 8; ++kc) qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qp + 16 * kc);
+    for (int kc = 0; kc < 8; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(qp + 16 * kc);
   }
   // the Q loads complete here, before any tile load is issued (otherwise the
-  // compiler's wait for them would also wait for the tile loads, in the loop)
+  // compiler's wait for them would also wait for the tile loads)
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-  // scores in log2 units straight from the matrix core: q * log2(e)/sqrt(d),
-  // rounded to bf16 once (a relative error of at most 2^-9 per element, the
-  // size of q's own rounding)
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int kc = 0; kc < 8; ++kc) {
-      typedef float f32x8 __attribute__((ext_vector_type(8)));
-      const f32x8 f = __builtin_convertvector(qf[qb][kc], f32x8) * scale_log2;
-      qf[qb][kc] = __builtin_convertvector(f, bf16x8);
-    }
+  for (int kc = 0; kc < 8; ++kc) {
+    typedef float f32x8 __attribute__((ext_vector_type(8)));
+    const f32x8 f = __builtin_convertvector(qf[kc], f32x8) * scale_log2;
+    qf[kc] = __builtin_convertvector(f, bf16x8);
+  }
 
-  // ---- global -> LDS.  A tile (K or V) is 8 pieces of 1 KiB = 4 key rows of
-  // 256 B; wave w loads pieces 2 w, 2 w + 1 of both.  Lane i of piece p
+  // ---- global -> LDS.  A tile (K or V) is 16 pieces of 1 KiB = 4 key rows
+  // of 256 B; wave w loads pieces 2 w, 2 w + 1 of both.  Lane i of piece p
   // fills LDS chunk i of the piece: row 4 p + i / 16, physical chunk i % 16,
   // which holds logical chunk (i % 16) ^ swizzle(row):
   //   K: swizzle(row) = row % 16   (fragment reads of 16 rows at one chunk)
@@ -207,6 +187,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     v_voff[u] = (uint32_t)(row * (int)vs * 2 + ((pc ^ (4 * (row & 3))) << 4));
   }
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_char*)smem;
+  // rows past the request's last key read as zero (descriptor bound)
   auto issue = [&](int t) __attribute__((always_inline)) {
     const int kb = t * BKV;
     const u32x4 kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
@@ -220,7 +201,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   };
 
   // ---- fragment addresses inside a slot
-  // K (A operand of S^T): row fr, logical chunk 2 kc + fh:
+  // K (A operand of S^T): key row 32 hb + fr, logical chunk 2 kc + fh:
   //   fr * 256 + (((2 kc + fh) ^ (fr % 16)) << 4) = k_lane ^ (kc << 5)
   const int k_lane = fr * 256 + ((fh ^ (fr & 15)) << 4);
   // V^T (A operand of O^T) by transposing reads.  Lanes 16 g .. 16 g + 15
@@ -237,12 +218,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   }
 
   const int n_tiles = (n_k + BKV - 1) / BKV;
-  const bool ragged = n_k % BKV != 0;
-  // Scores of one query block of a tile: S[4 i + j] = S[key 8 i + 4 fh + j][query 32 qb + fr]
-  f32x16 sq[2];         // sq[qb]: scores of the query block being computed or softmaxed
-  bf16x8 pq[2][2];      // pq[qb][kc]: P^T operand, probabilities of scores 8 kc .. 8 kc + 7
-  f32x16 oacc[4][2];    // oacc[db][qb][4 i + j] = O[query 32 qb + fr][d 32 db + 8 i + 4 fh + j]
-  // Softmax reference of the lane's rows (log2 units): P = 2^(score - m_ref).
+  // Scores of a tile: sq[hb][4 i + j] = S[key 32 hb + 8 i + 4 fh + j][query 32 wave + fr]
+  f32x16 sq[2];
+  bf16x8 pq[4];         // pq[kc]: P^T operand of keys 16 kc .. 16 kc + 15 (scores 8 (kc % 2) .. +7 of half kc / 2)
+  f32x16 oacc[4];       // oacc[db][4 i + j] = O[query 32 wave + fr][d 32 db + 8 i + 4 fh + j]
+  // Softmax reference of the lane's row (log2 units): P = 2^(score - m_ref).
   // It is fixed for the whole pass (no O rescale inside the loop).  The first
   // pass takes the first tile's row max and checks afterwards that every row
   // sum l stayed <= 2^kHeadroom (then every probability did, and O cannot
@@ -250,269 +230,182 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // raised by log2(l) when l is finite, which caps its probabilities at 1;
   // that pass also tracks x_max = max(score - m_ref), so a row whose sum had
   // overflowed gets m_ref = its exact max in a last pass.
-  float m_ref[2], x_max[2];
-  f32x16 nref[2];       // nref[qb]: -m_ref[qb] in every element, the bias of S
-  float l_run[2][2];    // this lane's share of the row sums, two partial sums per block
+  float m_ref = 0.f, x_max = -INFINITY;
+  float l_run[2];       // this lane's share of the row sum, two partial sums
+  f32x16 nref;          // -m_ref in every element, the bias of S
 
-  // keys past the request end (ragged last tile) score -inf
-  auto mask = [&](int t, f32x16& a) __attribute__((always_inline)) {
+  // S(t) for both 32-key halves (two independent chains); FIRST: from zero
+  auto S = [&](int t, auto first) __attribute__((always_inline)) {
+    const int so = (t % kRing) * kSlotBytes + k_lane;
+    bf16x8 ka[8], kb[8];
+    ka[0] = *reinterpret_cast<const bf16x8*>(smem + so);
+    kb[0] = *reinterpret_cast<const bf16x8*>(smem + so + 32 * 256);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = t * BKV + 8 * (v >> 2) + 4 * fh + (v & 3);
-      if (key >= n_k) a[v] = -INFINITY;
+    for (int kc = 0; kc < 8; ++kc) {
+      if (kc + 1 < 8) {
+        ka[kc + 1] = *reinterpret_cast<const bf16x8*>(smem + (so ^ ((kc + 1) << 5)));
+        kb[kc + 1] = *reinterpret_cast<const bf16x8*>(smem + (so ^ ((kc + 1) << 5)) + 32 * 256);
+      }
+      if (kc > 0) {
+        mfma_s_acc(sq[0], ka[kc], qf[kc]);
+        mfma_s_acc(sq[1], kb[kc], qf[kc]);
+      } else if (decltype(first)::value) {
+        mfma_s_first(sq[0], ka[0], qf[0]);
+        mfma_s_first(sq[1], kb[0], qf[0]);
+      } else {
+        mfma_s_bias(sq[0], ka[0], qf[0], nref);
+        mfma_s_bias(sq[1], kb[0], qf[0], nref);
+      }
     }
+    score_guard(sq[0]);
+    score_guard(sq[1]);
   };
-  // softmax pair j (0 .. 7) of query block qb: scores 2 j, 2 j + 1 -> pq[qb][j / 4]
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  auto soft_pair = [&](int qb, int j, auto track) __attribute__((always_inline)) {
-    const int kc = j >> 2, e = 2 * (j & 3);
-    const float x0 = sq[qb][2 * j], x1 = sq[qb][2 * j + 1];   // score - m_ref, log2 units
-    if (decltype(track)::value) x_max[qb] = fmaxf(fmaxf(x_max[qb], x0), x1);
-    const float p0 = __builtin_amdgcn_exp2f(x0), p1 = __builtin_amdgcn_exp2f(x1);
-    const bf16x2 pr = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
-    pq[qb][kc][e] = pr[0];
-    pq[qb][kc][e + 1] = pr[1];
-    // fp32 row sums with plain adds into two independent partial sums (a
-    // bf16 dot-product accumulation here stalls against the MFMAs)
-    l_run[qb][0] += p0;
-    l_run[qb][1] += p1;
-  };
-  // the softmax results of a half step are computed before its end, not sunk
-  // into the next half step (where the compiler would otherwise move them)
-  auto fence_soft = [&](int qb) __attribute__((always_inline)) {
-    asm volatile("" :: "v"(pq[qb][0]), "v"(pq[qb][1]), "v"(l_run[qb][0]), "v"(l_run[qb][1]), "v"(x_max[qb]));
-  };
-  auto v_frag = [&](int so, int m) __attribute__((always_inline)) {   // V^T fragment m = 4 kc + db of a slot
-    const int ad = so + (v_lane ^ ((m & 3) << 6)) + (m >> 2) * 16 * 256;
-    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad));
-    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad + 8 * 256));
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  };
-  // steady state (step t loaded tile t + kRing - 1 < n_tiles): tiles up to
-  // t + 2 are needed next, so kRing - 3 tiles may stay in flight
-  auto end_of_step_steady = [&]() __attribute__((always_inline)) {
-    wait_vmcnt<(kRing - 3) * kLoadsPerTile>();
-    __syncthreads();
-  };
-  auto end_of_step = [&](int t) __attribute__((always_inline)) {
-    // tiles up to t + 2 in LDS for the next step (V(t + 1), K(t + 2)); tiles
-    // up to t + kRing - 1 have been issued
-    wait_tiles(min(t + kRing - 1, n_tiles - 1) - min(t + 2, n_tiles - 1));
-    __syncthreads();
-  };
-
-  // Step t, two halves of 8 slots (half h works on query block h):
-  //   slot 8 h + i: one MFMA of S(t + 1) for block h (d-chunk i)
-  //                 one MFMA of O += V(t) P(t) for block h (V^T fragment i)
-  //                 softmax pair i of the other block's scores:
-  //                   half 0: S(t) block 1 -> P(t) block 1 (used by half 1)
-  //                   half 1: S(t + 1) block 0 (just computed) -> P(t + 1) block 0
-  // K and V^T fragments are read in half 0, 2 and 1 slots ahead, and kept for
-  // half 1.  Only one score block per query block is live at any time.
-  //   WITH_S: compute S(t + 1)  (false for the last tile)
-  //   MASKED: tile t + 1 is the ragged last tile
-  auto step = [&](int t, auto with_s, auto masked, int load_tile, auto track) __attribute__((always_inline)) {
-    constexpr bool WS = decltype(with_s)::value;
-    constexpr bool MK = decltype(masked)::value;
-    u32x4 kd{}, vd{};
-    uint32_t st = 0;
-    if (load_tile >= 0) {
-      const int kb = load_tile * BKV;
-      kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
-      vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
-      st = lds_base + (uint32_t)((load_tile % kRing) * kSlotBytes) + kPieces * wave * 1024;
-    }
-    const int so_k = ((t + 1) % kRing) * kSlotBytes + k_lane;
-    const int so_v = (t % kRing) * kSlotBytes;
-    bf16x8 kf[8], vf[8];
-    if (WS) {
-      kf[0] = *reinterpret_cast<const bf16x8*>(smem + so_k);
-      kf[1] = *reinterpret_cast<const bf16x8*>(smem + (so_k ^ (1 << 5)));
-    }
-    vf[0] = v_frag(so_v, 0);
-    score_guard(sq[1]);   // S(t) block 1 was finished at the end of the previous step
-    __builtin_amdgcn_sched_barrier(0);
+  // P(t) from S(t).  FIRST: S(t) came from zero (the reference is set, in the
+  // first pass, and subtracted here); LAST: keys past the request end -> -inf
+  auto softmax = [&](int t, auto first, auto last, auto track) __attribute__((always_inline)) {
+    if (decltype(last)::value && n_k % BKV != 0) {
 #pragma unroll
-    for (int sl = 0; sl < 16; ++sl) {
-      const int h = sl >> 3, i = sl & 7;
-      if (h == 0) {
-        if (WS && i + 2 < 8) kf[i + 2] = *reinterpret_cast<const bf16x8*>(smem + (so_k ^ ((i + 2) << 5)));
-        if (i + 1 < 8) vf[i + 1] = v_frag(so_v, i + 1);
-      }
-      if (WS) {
-        if (i == 0) mfma_s_bias(sq[h], kf[i], qf[h][i], nref[h]);
-        else mfma_s_acc(sq[h], kf[i], qf[h][i]);
-      }
-      oacc[i & 3][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pq[h][i >> 2], oacc[i & 3][h], 0, 0, 0);
-      if (sl == 8) {
-        // S(t + 1) block 0 is complete: mask it if it is the ragged last tile,
-        // then wait out the matrix-core latency before reading it
-        if (MK && ragged) mask(t + 1, sq[0]);
-        score_guard(sq[0]);
-      }
-      if (h == 0) soft_pair(1, i, track);
-      else if (WS) soft_pair(0, i, track);
-      if (load_tile >= 0 && (sl & 3) == 1) {
-        const int u = sl >> 3, v = (sl >> 2) & 1;   // K piece 0, V piece 0, K piece 1, V piece 1
-        if (v == 0) load_lds16(kd, k_voff[u], st + u * 1024);
-        else load_lds16(vd, v_voff[u], st + kTileBytes + u * 1024);
-      }
-      if (sl == 7) fence_soft(1);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = t * BKV + 32 * hb + 8 * (v >> 2) + 4 * fh + (v & 3);
+          if (key >= n_k) sq[hb][v] = -INFINITY;
+        }
     }
-    if (WS) {
-      fence_soft(0);
-      if (MK && ragged) {
-        score_guard(sq[1]);
-        mask(t + 1, sq[1]);
+    if (decltype(first)::value) {
+      if (!decltype(track)::value) {
+        // first pass: the reference is the row max of the first tile
+        float mx = fmaxf(sq[0][0], sq[1][0]);
+#pragma unroll
+        for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(sq[0][v], sq[1][v]));
+        auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        m_ref = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
       }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        sq[0][v] -= m_ref;
+        sq[1][v] -= m_ref;
+        nref[v] = -m_ref;
+      }
+    }
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int jp = 0; jp < 8; ++jp) {
+        const float x0 = sq[hb][2 * jp], x1 = sq[hb][2 * jp + 1];   // score - m_ref, log2 units
+        if (decltype(track)::value) x_max = fmaxf(fmaxf(x_max, x0), x1);
+        const float p0 = __builtin_amdgcn_exp2f(x0), p1 = __builtin_amdgcn_exp2f(x1);
+        const bf16x2 pr = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
+        pq[2 * hb + (jp >> 2)][2 * (jp & 3)] = pr[0];
+        pq[2 * hb + (jp >> 2)][2 * (jp & 3) + 1] = pr[1];
+        l_run[0] += p0;
+        l_run[1] += p1;
+      }
+  };
+  auto PV = [&](int t) __attribute__((always_inline)) {
+    const int so = (t % kRing) * kSlotBytes;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const int ad = so + (v_lane ^ (db << 6)) + kc * 16 * 256;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((lds_char*)smem + ad + 8 * 256));
+        const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pq[kc], oacc[db], 0, 0, 0);
+      }
+  };
+  // One step: S(t), P(t), O += V(t) P(t); then tile t + 1 must be in LDS for
+  // every wave (a wave's loads of tile t + 2 may stay in flight), and tile
+  // t + 3 goes into the slot of tile t - 1, which every wave has finished.
+  auto step = [&](int t, auto first, auto last, auto track) __attribute__((always_inline)) {
+    S(t, first);
+    softmax(t, first, last, track);
+    PV(t);
+    if (!decltype(last)::value) {
+      if (t + 2 < n_tiles) wait_vmcnt<kLoadsPerTile>();
+      else wait_vmcnt<0>();
+      __syncthreads();
+      if (t + 3 < n_tiles) issue(t + 3);
     }
   };
   using kOn = std::true_type;
   using kOff = std::false_type;
-
-  __shared__ int redo_flag[2];   // one flag per pass that may ask for another
-  if (tid < 2) redo_flag[tid] = 0;
   auto run_pass = [&](auto track) __attribute__((always_inline)) {
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = f32x16{};
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      l_run[qb][0] = l_run[qb][1] = 0.f;
-      x_max[qb] = -INFINITY;
-    }
-    const int n_pre = min(kRing, n_tiles);
+    for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
+    l_run[0] = l_run[1] = 0.f;
+    x_max = -INFINITY;
+    const int n_pre = min(3, n_tiles);
     for (int t = 0; t < n_pre; ++t) issue(t);
-    // tiles 0 and 1 in LDS (K(0), K(1), V(0))
-    wait_tiles(n_pre - 1 - min(1, n_tiles - 1));
+    // tile 0 in LDS
+    if (n_pre == 3) wait_vmcnt<2 * kLoadsPerTile>();
+    else if (n_pre == 2) wait_vmcnt<kLoadsPerTile>();
+    else wait_vmcnt<0>();
     __syncthreads();
-
-    if (n_tiles > 0) {
-      // S(0), both query blocks
-      {
-        const int so = k_lane;
-#pragma unroll
-        for (int kc = 0; kc < 8; ++kc) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(smem + (so ^ (kc << 5)));
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            if (kc == 0) mfma_s_first(sq[qb], kf, qf[qb][kc]);
-            else mfma_s_acc(sq[qb], kf, qf[qb][kc]);
-          }
-        }
-        score_guard(sq[0]);
-        score_guard(sq[1]);
-      }
-      if (n_tiles == 1 && ragged) {
-        mask(0, sq[0]);
-        mask(0, sq[1]);
-      }
-      if (!decltype(track)::value) {
-        // first pass: the reference is the row max of the first tile
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          float mx = sq[qb][0];
-#pragma unroll
-          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sq[qb][v]);
-          auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          m_ref[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-        }
-      }
-      // S(0) was computed from zero: subtract the reference here; the later
-      // tiles start from it
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          sq[qb][v] -= m_ref[qb];
-          nref[qb][v] = -m_ref[qb];
-        }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) soft_pair(0, j, track);   // P(0) block 0
+    if (n_tiles == 1) {
+      step(0, kOn{}, kOn{}, track);
+    } else {
+      step(0, kOn{}, kOff{}, track);
+      // no compiler-tracked load may still be pending when the loop starts:
+      // its tracking would otherwise put a vmcnt wait (which also waits for
+      // the tile loads in flight) at the top of every iteration
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
+      for (int t = 1; t + 1 < n_tiles; ++t) step(t, kOff{}, kOff{}, track);
+      step(n_tiles - 1, kOff{}, kOn{}, track);
     }
-    // Step t loads tile t + kRing - 1 into the slot of tile t - 1 (free since
-    // the barrier that ended step t - 1); step 0 has nothing to load, the
-    // prologue filled every slot.
-    int t = 0;
-    if (t + 2 < n_tiles) {
-      step(0, kOn{}, kOff{}, -1, track);
-      end_of_step(0);
-      t = 1;
-    }
-    // no compiler-tracked load may still be pending when the steady loop
-    // starts: its tracking would otherwise put a vmcnt wait (which also waits
-    // for the tile loads in flight) at the top of every iteration
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
-    for (; t + kRing < n_tiles; ++t) {      // loads every step, constant wait count
-      step(t, kOn{}, kOff{}, t + kRing - 1, track);
-      end_of_step_steady();
-    }
-    for (; t + 2 < n_tiles; ++t) {
-      step(t, kOn{}, kOff{}, t + kRing - 1 < n_tiles ? t + kRing - 1 : -1, track);
-      end_of_step(t);
-    }
-    if (t + 1 < n_tiles) {   // S of the last tile (t + 1), which may be ragged
-      step(t, kOn{}, kOn{}, -1, track);
-      end_of_step(t);
-      ++t;
-    }
-    if (t < n_tiles) step(t, kOff{}, kOff{}, -1, track);   // the last tile: PV only
   };
 
-  // this lane's rows: row sums (the lanes l and l + 32 hold halves) and x_max
-  auto row_sum = [&](int qb) __attribute__((always_inline)) {
-    const float l_lane = l_run[qb][0] + l_run[qb][1];
+  // this lane's row: row sum (the lanes l and l + 32 hold halves) and x_max
+  auto row_sum = [&]() __attribute__((always_inline)) {
+    const float l_lane = l_run[0] + l_run[1];
     auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_lane), __float_as_uint(l_lane), false, false);
     return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
   };
-  auto row_xmax = [&](int qb) __attribute__((always_inline)) {
-    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x_max[qb]), __float_as_uint(x_max[qb]), false, false);
+  auto row_xmax = [&]() __attribute__((always_inline)) {
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x_max), __float_as_uint(x_max), false, false);
     return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
   };
   constexpr float kMaxSum = 18446744073709551616.0f;   // 2^kHeadroom
-  run_pass(kOff{});
-  {
-    const float l0 = row_sum(0), l1 = row_sum(1);
-    const bool over = !(l0 <= kMaxSum) || !(l1 <= kMaxSum);   // also true for inf / NaN
+  if (n_tiles > 0) {
+    run_pass(kOff{});
+    const float l0 = row_sum();
+    const bool over = !(l0 <= kMaxSum);   // also true for inf / NaN
     if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) redo_flag[0] = 1;
     __syncthreads();
     if (__builtin_amdgcn_readfirstlane(redo_flag[0]) != 0) {
       // finite sums: probabilities <= 1 after the shift (l >= 2^x_max)
-      if (l0 > kMaxSum && l0 <= FLT_MAX) m_ref[0] += __log2f(l0);
-      if (l1 > kMaxSum && l1 <= FLT_MAX) m_ref[1] += __log2f(l1);
+      if (l0 > kMaxSum && l0 <= FLT_MAX) m_ref += __log2f(l0);
       for (int pass = 1;; ++pass) {
         run_pass(kOn{});
         if (pass == 2) break;
-        const float xm0 = row_xmax(0), xm1 = row_xmax(1);
-        const bool over2 = xm0 > kHeadroom || xm1 > kHeadroom;
-        if (__builtin_amdgcn_ballot_w64(over2) != 0 && lane == 0) redo_flag[1] = 1;
+        const float xm = row_xmax();
+        if (__builtin_amdgcn_ballot_w64(xm > kHeadroom) != 0 && lane == 0) redo_flag[1] = 1;
         __syncthreads();
         if (__builtin_amdgcn_readfirstlane(redo_flag[1]) == 0) break;
-        m_ref[0] += xm0;   // the exact row max: every x <= 0
-        m_ref[1] += xm1;
+        m_ref += xm;   // the exact row max: every x <= 0
       }
     }
+  } else {
+#pragma unroll
+    for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
+    l_run[0] = l_run[1] = 0.f;
   }
 
   // ---- normalise and store
+  const float l_tot = row_sum();
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
+  if (my_q < q_end) {
+    bf16* op = O + (int64_t)my_q * os + head * D + 4 * fh;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const float l_tot = row_sum(qb);
-    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
-    if (my_q[qb] < q_end) {
-      bf16* op = O + (int64_t)my_q[qb] * os + head * D + 4 * fh;
+    for (int db = 0; db < 4; ++db)
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
+      for (int i = 0; i < 4; ++i) {
+        bf16x4 ov;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          bf16x4 ov;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) ov[j] = (bf16)(oacc[db][qb][4 * i + j] * inv);
-          *reinterpret_cast<bf16x4*>(op + 32 * db + 8 * i) = ov;
-        }
-    }
+        for (int jj = 0; jj < 4; ++jj) ov[jj] = (bf16)(oacc[db][4 * i + jj] * inv);
+        *reinterpret_cast<bf16x4*>(op + 32 * db + 8 * i) = ov;
+      }
   }
 }
 
