@@ -231,7 +231,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // that pass also tracks x_max = max(score - m_ref), so a row whose sum had
   // overflowed gets m_ref = its exact max in a last pass.
   float m_ref = 0.f, x_max = -INFINITY;
-  float l_run[2];       // this lane's share of the row sum, two partial sums
+  float l_run[4];       // this lane's share of the row sum, four partial sums
   f32x16 nref;          // -m_ref in every element, the bias of S
 
   // S(t) for both 32-key halves (two independent chains); FIRST: from zero
@@ -298,8 +298,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
         const bf16x2 pr = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
         pq[2 * hb + (jp >> 2)][2 * (jp & 3)] = pr[0];
         pq[2 * hb + (jp >> 2)][2 * (jp & 3) + 1] = pr[1];
-        l_run[0] += p0;
-        l_run[1] += p1;
+        l_run[2 * (jp & 1)] += p0;
+        l_run[2 * (jp & 1) + 1] += p1;
       }
   };
   auto PV = [&](int t) __attribute__((always_inline)) {
@@ -334,7 +334,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   auto run_pass = [&](auto track) __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
-    l_run[0] = l_run[1] = 0.f;
+    l_run[0] = l_run[1] = l_run[2] = l_run[3] = 0.f;
     x_max = -INFINITY;
     const int n_pre = min(3, n_tiles);
     for (int t = 0; t < n_pre; ++t) issue(t);
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
 
   // this lane's row: row sum (the lanes l and l + 32 hold halves) and x_max
   auto row_sum = [&]() __attribute__((always_inline)) {
-    const float l_lane = l_run[0] + l_run[1];
+    const float l_lane = (l_run[0] + l_run[1]) + (l_run[2] + l_run[3]);
     auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_lane), __float_as_uint(l_lane), false, false);
     return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
   };
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   } else {
 #pragma unroll
     for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
-    l_run[0] = l_run[1] = 0.f;
+    l_run[0] = l_run[1] = l_run[2] = l_run[3] = 0.f;
   }
 
   // ---- normalise and store
