@@ -112,8 +112,14 @@ def cpu_baseline(wl, target_s=12.0):
             + 2.0 * wl.txt_len * D * 2 * D + 2.0 * (D * wl.freq_dim + 7 * D * D)
         return dt, fl
 
-    dt, fl = run(min(16, n_all))
-    n = int(min(4096, n_all, max(16, 16 * target_s / max(dt, 1e-3))))
+    # two probes give the fixed cost (conditioning, text projection) and the
+    # cost per sampled row, so the sample lands near target_s
+    n1, n2 = min(16, n_all), min(64, n_all)
+    dt1, _ = run(n1)
+    dt2, _ = run(n2)
+    per_row = max((dt2 - dt1) / max(n2 - n1, 1), 1e-6)
+    fixed = max(dt1 - n1 * per_row, 0.0)
+    n = int(min(4096, n_all, max(n2, (target_s - fixed) / per_row)))
     dt, fl = run(n)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": (f"{wl.name}: all block steps for {n} evenly spaced query rows of the "
