@@ -159,7 +159,8 @@ dit_status dit_timestep_modulation(const dit_block_config *cfg, const dit_block_
  * rows cu_q[r]..cu_q[r+1] and keys/values rows cu_k[r]..cu_k[r+1] (host
  * arrays; cu_q == cu_k for self-attention).  Head h of row i starts at
  * q + i*q_row_stride + h*head_dim (strides in elements; likewise k, v, o).
- * o must not overlap q, k or v.  bf16 needs head_dim 128; fp32 takes 64 or 128. */
+ * o must not overlap q, k or v.  bf16 needs head_dim 128; fp32 takes 64 or 128.
+ * A request with queries but no keys gets rows of zeros. */
 dit_status dit_attention_varlen(const void *q, const void *k, const void *v, void *o,
                                 int64_t q_row_stride, int64_t k_row_stride,
                                 int64_t v_row_stride, int64_t o_row_stride,

@@ -219,6 +219,27 @@ def test_attention_varlen(dtype, H, d, lq, lk):
     check(host(out), ref, dtype, "attention")
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_attention_request_without_keys(dtype, d):
+    """A request with queries but no keys gets rows of zeros; the packed
+    request beside it still matches the oracle (its keys start at row 0)."""
+    B = require_gpu()
+    log(f"case attention without keys {dtype} d={d}")
+    H, lq, lk = 2, [50, 30], [0, 70]
+    cu_q, cu_k = _cu(lq), _cu(lk)
+    W = H * d
+    qb = synth.draw((80, 3 * W), (32, H, 80, 70), dtype)
+    kvb = synth.draw((70, 2 * W), (33, H, 80, 70), dtype)
+    qt, kvt = dev(qb), dev(kvb)
+    out = dev(np.full((80, W), 7.0, dtype=np.float32)).to(qt.dtype)   # poison: every row is written
+    B.attention_varlen(qt[:, :W], kvt[:, :W], kvt[:, W:], out, cu_q, cu_k, H, d)
+    torch.cuda.synchronize()
+    got = host(out)
+    assert np.all(got[:50] == 0.0)
+    ref = O.attention_varlen(O.decode(qb)[50:, :W], O.decode(kvb)[:, :W], O.decode(kvb)[:, W:], [0, 30], [0, 70], H, d)
+    check(got[50:], ref, dtype, "attention")
+
+
 @pytest.mark.parametrize("jump_key,big_val", [(100, 20.0), (1999, 20.0), (1500, 10.0)])
 def test_attention_late_score_jump(jump_key, big_val):
     """A key far past the first tile whose score exceeds every earlier one by
