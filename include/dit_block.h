@@ -46,7 +46,7 @@ extern "C" {
 #endif
 
 #define DIT_MAX_REQ 64
-#define DIT_ABI_VERSION 2
+#define DIT_ABI_VERSION 3
 
 typedef enum {
   DIT_OK = 0,
@@ -125,23 +125,34 @@ dit_status dit_block_forward(const dit_block_config *cfg, const dit_block_weight
                              const float *mod, const void *txt, void *y, void *ws,
                              size_t ws_bytes, hipStream_t stream);
 
-/* Steps before self-attention, on this GPU's rows: conditioning mod = adaLN(t)
- * (device fp32 [n_req, 6, D], written), modulated LayerNorm, QKV projection,
- * per-head RMSNorm and rotary on q and k.  qkv: [rows, 3D] with q in columns
- * [0,D), k in [D,2D), v in [2D,3D), head j at j*d within each (written). */
+/* The block split at self-attention, the two points where a sequence-parallel
+ * runtime exchanges rows for heads (an all-to-all each way) between GPUs.
+ * Both halves take the conditioning the way dit_block_forward does: either
+ * timesteps t (the block's own timestep MLP and adaLN projection run) or
+ * precomputed modulation vectors (a model whose blocks share one timestep
+ * MLP; w_t1..b_ada are then not read).
+ *
+ * Steps before self-attention, on this GPU's rows: modulated LayerNorm, QKV
+ * projection, per-head RMSNorm and rotary on q and k.  With t != NULL (device
+ * fp32 [n_req]) the modulation mod = adaLN(t) is computed and written to mod
+ * (device fp32 [n_req, 6, D]); with t == NULL, mod is read as given.
+ * qkv: [rows, 3D] with q in columns [0,D), k in [D,2D), v in [2D,3D), head j
+ * at j*d within each (written). */
 dit_status dit_block_pre_attention(const dit_block_config *cfg, const dit_block_weights *w,
                                    const dit_varlen *vl, const void *x, const float *t,
                                    float *mod, void *qkv, void *ws, size_t ws_bytes,
                                    hipStream_t stream);
 
 /* Steps after self-attention, on this GPU's rows: o [rows, D] is the
- * attention output (heads concatenated), mod the modulation from
- * dit_block_pre_attention or dit_timestep_modulation.  Gated output projection,
- * cross-attention to each request's text, gated GELU-tanh MLP; writes y. */
+ * attention output (heads concatenated).  Gated output projection,
+ * cross-attention to each request's text, gated GELU-tanh MLP; writes y.
+ * mod: device fp32 [n_req, 6, D] (from dit_block_pre_attention or
+ * dit_timestep_modulation), or NULL to compute it from t (device fp32
+ * [n_req]) in the workspace.  y may equal x. */
 dit_status dit_block_post_attention(const dit_block_config *cfg, const dit_block_weights *w,
                                     const dit_varlen *vl, const void *x, const void *o,
-                                    const void *txt, const float *mod, void *y, void *ws,
-                                    size_t ws_bytes, hipStream_t stream);
+                                    const void *txt, const float *t, const float *mod, void *y,
+                                    void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* --------------------------------------------------------------- the stages */
 
@@ -159,8 +170,12 @@ dit_status dit_timestep_modulation(const dit_block_config *cfg, const dit_block_
  * rows cu_q[r]..cu_q[r+1] and keys/values rows cu_k[r]..cu_k[r+1] (host
  * arrays; cu_q == cu_k for self-attention).  Head h of row i starts at
  * q + i*q_row_stride + h*head_dim (strides in elements; likewise k, v, o).
- * o must not overlap q, k or v.  bf16 needs head_dim 128; fp32 takes 64 or 128.
- * A request with queries but no keys gets rows of zeros. */
+ * softmax_scale 0 selects the standard 1/sqrt(head_dim); any other finite
+ * value is used as given (inf or NaN: DIT_ERR_INVALID_ARG).  o must not
+ * overlap q, k or v: the byte range from o's first to its last row must not
+ * meet that of q, k or v (checked, DIT_ERR_INVALID_ARG); q, k and v may share
+ * one buffer.  bf16 needs head_dim 128; fp32 takes 64 or 128.  A request with
+ * queries but no keys gets rows of zeros. */
 dit_status dit_attention_varlen(const void *q, const void *k, const void *v, void *o,
                                 int64_t q_row_stride, int64_t k_row_stride,
                                 int64_t v_row_stride, int64_t o_row_stride,

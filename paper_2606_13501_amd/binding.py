@@ -134,7 +134,7 @@ def lib() -> ctypes.CDLL:
         "dit_block_workspace_size": (sz, [PC, PV]),
         "dit_block_forward": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_block_pre_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
-        "dit_block_post_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "dit_block_post_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_timestep_modulation": (i32, [PC, PW, i32, vp, vp, vp, sz, vp]),
         "dit_attention_varlen": (i32, [vp, vp, vp, vp, i64, i64, i64, i64, PI, PI, i32, i32, i32, f32, i32, vp]),
         "dit_adaln_modulate": (i32, [vp, vp, vp, i64, PI, i32, i32, f32, vp, i32, vp]),
@@ -266,14 +266,16 @@ def block_forward(cfg, weights: CWeights, vl, x, t, txt, y, ws, stream=None, mod
 
 
 def block_pre_attention(cfg, weights, vl, x, t, mod, qkv, ws, stream=None):
+    """t given: mod is written from t; t None: mod is read."""
     _check(lib().dit_block_pre_attention(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
                                          _ptr(t), _ptr(mod), _ptr(qkv), _ptr(ws), ws.numel() * ws.element_size(),
                                          _stream(stream)), "dit_block_pre_attention")
 
 
-def block_post_attention(cfg, weights, vl, x, o, txt, mod, y, ws, stream=None):
+def block_post_attention(cfg, weights, vl, x, o, txt, mod, y, ws, stream=None, t=None):
+    """mod None: the modulation is computed from t."""
     _check(lib().dit_block_post_attention(ctypes.byref(cfg.c), ctypes.byref(weights), ctypes.byref(vl.c), _ptr(x),
-                                          _ptr(o), _ptr(txt), _ptr(mod), _ptr(y), _ptr(ws),
+                                          _ptr(o), _ptr(txt), _ptr(t), _ptr(mod), _ptr(y), _ptr(ws),
                                           ws.numel() * ws.element_size(), _stream(stream)),
            "dit_block_post_attention")
 
@@ -285,8 +287,9 @@ def timestep_modulation(cfg, weights, t, mod, ws, stream=None):
 
 
 def attention_varlen(q, k, v, o, cu_q, cu_k, n_heads, head_dim, softmax_scale=None, stream=None):
+    """softmax_scale None: the library's default, 1/sqrt(head_dim)."""
     cq, ck = _i32(cu_q), _i32(cu_k)
-    scale = softmax_scale if softmax_scale is not None else head_dim ** -0.5
+    scale = 0.0 if softmax_scale is None else softmax_scale
     _check(lib().dit_attention_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(o), q.stride(0), k.stride(0), v.stride(0),
                                       o.stride(0), _pi(cq), _pi(ck), len(cq) - 1, n_heads, head_dim, scale,
                                       dtype_code(q.dtype), _stream(stream)), "dit_attention_varlen")

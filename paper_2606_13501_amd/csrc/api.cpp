@@ -1,6 +1,7 @@
 // C ABI of the DiT block library: argument validation on the host (before
 // any HIP call), workspace layout, and the order of launches of one block.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -67,6 +68,17 @@ dit_status check_cu(const int32_t* cu, int n_req, const char* name) {
     if (cu[r + 1] < cu[r]) return fail(DIT_ERR_INVALID_ARG, "%s decreases at %d", name, r);
   return DIT_OK;
 }
+
+// Byte range [lo, hi) of `rows` rows of `width` elements at a row stride.
+struct Span { uintptr_t lo, hi; };
+
+Span span(const void* p, int64_t rows, int64_t stride, int64_t width, int64_t es) {
+  const uintptr_t lo = (uintptr_t)p;
+  if (rows <= 0) return {lo, lo};
+  return {lo, lo + (uintptr_t)(((rows - 1) * stride + width) * es)};
+}
+
+bool overlaps(const Span& a, const Span& b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
 
 ReqTable make_req(const int32_t* cu, int n_req) {
   ReqTable t;
@@ -150,6 +162,15 @@ dit_status check_cfg(const dit_block_config* c) {
       return fail(DIT_ERR_UNSUPPORTED, "fp32 needs hidden, mlp_hidden and freq_dim multiples of 4");
     if (c->hidden > 4096) return fail(DIT_ERR_UNSUPPORTED, "fp32 hidden %d > 4096", c->hidden);
   }
+  return DIT_OK;
+}
+
+// The block's own conditioning chain: timestep MLP and adaLN projection.
+dit_status check_cond_weights(const dit_block_weights* w) {
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
+  DIT_TRY(check_ptr(w->w_t1, "w_t1")); DIT_TRY(check_ptr(w->b_t1, "b_t1"));
+  DIT_TRY(check_ptr(w->w_t2, "w_t2")); DIT_TRY(check_ptr(w->b_t2, "b_t2"));
+  DIT_TRY(check_ptr(w->w_ada, "w_ada")); DIT_TRY(check_ptr(w->b_ada, "b_ada"));
   return DIT_OK;
 }
 
@@ -564,40 +585,46 @@ dit_status dit_block_pre_attention(const dit_block_config* cfg, const dit_block_
                                    const void* x, const float* t, float* mod, void* qkv, void* ws, size_t ws_bytes,
                                    hipStream_t stream) {
   g_last_error.clear();
-  DIT_TRY(check_block_call(cfg, w, vl, true, false));
+  // with t: mod is written from the block's timestep MLP; without: mod is read
+  DIT_TRY(check_block_call(cfg, w, vl, true, false, t != nullptr));
   DIT_TRY(check_ptr(x, "x"));
-  DIT_TRY(check_ptr(t, "t"));
+  DIT_TRY(check_ptr(t, "t", true));
   DIT_TRY(check_ptr(mod, "mod"));
   DIT_TRY(check_ptr(qkv, "qkv"));
   Workspace W;
   DIT_TRY(check_ws(cfg, vl, ws, ws_bytes, &W));
-  DIT_TRY(run_cond(cfg, w, vl->n_req, t, mod, W.e, W.a1, W.c, stream));
+  if (t) DIT_TRY(run_cond(cfg, w, vl->n_req, t, mod, W.e, W.a1, W.c, stream));
   return pre_attention_impl(cfg, w, vl, x, mod, qkv, W, stream);
 }
 
 dit_status dit_block_post_attention(const dit_block_config* cfg, const dit_block_weights* w, const dit_varlen* vl,
-                                    const void* x, const void* o, const void* txt, const float* mod, void* y,
-                                    void* ws, size_t ws_bytes, hipStream_t stream) {
+                                    const void* x, const void* o, const void* txt, const float* t, const float* mod,
+                                    void* y, void* ws, size_t ws_bytes, hipStream_t stream) {
   g_last_error.clear();
   DIT_TRY(check_block_call(cfg, w, vl, false, true));
+  // without mod the modulation comes from t through the block's timestep MLP
+  if (!mod) DIT_TRY(check_cond_weights(w));
   DIT_TRY(check_ptr(x, "x"));
   DIT_TRY(check_ptr(o, "o"));
   DIT_TRY(check_ptr(txt, "txt"));
-  DIT_TRY(check_ptr(mod, "mod"));
+  if (mod) DIT_TRY(check_ptr(mod, "mod"));
+  else DIT_TRY(check_ptr(t, "t"));
   DIT_TRY(check_ptr(y, "y"));
   Workspace W;
   DIT_TRY(check_ws(cfg, vl, ws, ws_bytes, &W));
-  return post_attention_impl(cfg, w, vl, x, o, txt, mod, y, W, stream);
+  const float* m = mod;
+  if (!m) {
+    DIT_TRY(run_cond(cfg, w, vl->n_req, t, W.mod, W.e, W.a1, W.c, stream));
+    m = W.mod;
+  }
+  return post_attention_impl(cfg, w, vl, x, o, txt, m, y, W, stream);
 }
 
 dit_status dit_timestep_modulation(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
                                    const float* t, float* mod, void* ws, size_t ws_bytes, hipStream_t stream) {
   g_last_error.clear();
   DIT_TRY(check_cfg(cfg));
-  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
-  DIT_TRY(check_ptr(w->w_t1, "w_t1")); DIT_TRY(check_ptr(w->b_t1, "b_t1"));
-  DIT_TRY(check_ptr(w->w_t2, "w_t2")); DIT_TRY(check_ptr(w->b_t2, "b_t2"));
-  DIT_TRY(check_ptr(w->w_ada, "w_ada")); DIT_TRY(check_ptr(w->b_ada, "b_ada"));
+  DIT_TRY(check_cond_weights(w));
   if (n_req < 1 || n_req > DIT_MAX_REQ) return fail(DIT_ERR_INVALID_ARG, "n_req = %d outside 1..%d", n_req, DIT_MAX_REQ);
   DIT_TRY(check_ptr(t, "t"));
   DIT_TRY(check_ptr(mod, "mod"));
@@ -623,10 +650,12 @@ dit_status dit_attention_varlen(const void* q, const void* k, const void* v, voi
   DIT_TRY(check_cu(cu_q, n_req, "cu_q"));
   DIT_TRY(check_cu(cu_k, n_req, "cu_k"));
   if (n_heads < 1) return fail(DIT_ERR_INVALID_ARG, "n_heads = %d", n_heads);
-  if (!(softmax_scale > 0.f) && !(softmax_scale < 0.f) ) return fail(DIT_ERR_INVALID_ARG, "softmax_scale is 0 or NaN");
+  if (!isfinite(softmax_scale)) return fail(DIT_ERR_INVALID_ARG, "softmax_scale is not finite");
   if (dtype == DIT_BF16 && head_dim != 128) return fail(DIT_ERR_UNSUPPORTED, "bf16 attention head_dim %d (only 128)", head_dim);
   if (dtype == DIT_F32 && head_dim != 64 && head_dim != 128)
     return fail(DIT_ERR_UNSUPPORTED, "fp32 attention head_dim %d (64 or 128)", head_dim);
+  // 0 selects the standard scale 1/sqrt(head_dim)
+  const float scale = softmax_scale == 0.f ? 1.0f / sqrtf((float)head_dim) : softmax_scale;
   const int64_t width = (int64_t)n_heads * head_dim;
   const int64_t vec = dtype == DIT_BF16 ? 8 : 4;
   const int64_t strides[4] = {q_row_stride, k_row_stride, v_row_stride, o_row_stride};
@@ -634,9 +663,18 @@ dit_status dit_attention_varlen(const void* q, const void* k, const void* v, voi
     if (strides[i] < width || strides[i] % vec)
       return fail(DIT_ERR_INVALID_ARG, "row stride %lld: must be >= n_heads*head_dim = %lld and a multiple of %lld",
                   (long long)strides[i], (long long)width, (long long)vec);
+  // o is written while q, k and v are still being read: its byte range must
+  // not meet theirs (ranges from the first to the last byte a row touches)
+  const int64_t es = (int64_t)elem_size(dtype);
+  const Span so = span(o, cu_q[n_req], o_row_stride, width, es);
+  const Span in[3] = {span(q, cu_q[n_req], q_row_stride, width, es), span(k, cu_k[n_req], k_row_stride, width, es),
+                      span(v, cu_k[n_req], v_row_stride, width, es)};
+  const char* names[3] = {"q", "k", "v"};
+  for (int i = 0; i < 3; ++i)
+    if (overlaps(so, in[i])) return fail(DIT_ERR_INVALID_ARG, "o overlaps %s", names[i]);
   DIT_TRY(check_attn_items(cu_q, n_req, n_heads));
   return run_attention(q, k, v, o, q_row_stride, k_row_stride, v_row_stride, o_row_stride, make_req(cu_q, n_req),
-                       make_req(cu_k, n_req), n_heads, head_dim, softmax_scale, dtype, stream);
+                       make_req(cu_k, n_req), n_heads, head_dim, scale, dtype, stream);
 }
 
 dit_status dit_adaln_modulate(const void* x, const float* shift, const float* scale, int64_t mod_stride,

@@ -14,6 +14,7 @@ import torch
 import torch.nn.functional as F
 
 from oracle import dit_block as O
+import synth.gen as SG
 
 RNG = np.random.default_rng(20260613)
 
@@ -535,7 +536,81 @@ def check_block_composition_and_rows():
     _close(ks, k[6:9], 1e-14, "shard k")
 
 
+# ---------------------------------------------------------------- bf16 storage
+
+
+def _bits(words):
+    return np.array(words, dtype=np.uint16)
+
+
+def _f32(words):
+    return np.array(words, dtype=np.uint32).view(np.float32)
+
+
+def check_bf16_codec():
+    """The stored-value decoding every parity check reads through (oracle
+    ``decode``) and the encoder that writes the bf16 inputs both sides read
+    (``synth.gen.bf16_bits``).  bfloat16 is the top half of an IEEE binary32
+    word: sign, 8 exponent bits (bias 127), 7 mantissa bits; the encoder
+    rounds to nearest, ties to even.  Checked on hand-worked bit patterns and
+    against torch's own float32 -> bfloat16 conversion."""
+    # decode: hand-worked patterns
+    words = [0x3F80, 0xBF80, 0x4049, 0x3C00, 0x0000, 0x0001, 0x007F, 0x0080, 0x7F7F, 0x7F80, 0xFF80, 0xC2F7]
+    want = [1.0, -1.0, 3.140625, 2.0 ** -7, 0.0, 2.0 ** -133, 127 * 2.0 ** -133, 2.0 ** -126,
+            (2 - 2.0 ** -7) * 2.0 ** 127, math.inf, -math.inf, -123.5]
+    got = O.decode(_bits(words))
+    assert got.dtype == np.float64, f"decode gives {got.dtype}"
+    for wd, g, v in zip(words, got, want):
+        assert g == v, f"decode(0x{wd:04X}) = {g!r}, expected {v!r}"
+    neg0 = O.decode(_bits([0x8000]))[0]
+    assert neg0 == 0.0 and math.copysign(1.0, neg0) < 0, "decode(0x8000) is not -0.0"
+    # float32 storage decodes to itself
+    f = np.array([1.5, -2.25e-30, 3.0e38], dtype=np.float32)
+    assert np.array_equal(O.decode(f), f.astype(np.float64)), "float32 decode"
+    # encode: hand-worked round-to-nearest-even cases (float32 word -> bf16 word)
+    cases = [
+        (0x3F800000, 0x3F80),   # 1.0
+        (0x3F808000, 0x3F80),   # 1 + 2^-8: a tie, 0x3F80 is even
+        (0x3F818000, 0x3F82),   # 1 + 3*2^-8: a tie, 0x3F81 is odd -> up
+        (0x3F808001, 0x3F81),   # just above the tie
+        (0x3F807FFF, 0x3F80),   # just below the tie
+        (0xBF818000, 0xBF82),   # the odd tie, negative
+        (0x00010000, 0x0001),   # smallest bf16 subnormal
+        (0x00018000, 0x0002),   # subnormal tie -> even
+        (0x00008000, 0x0000),   # half the smallest subnormal: tie -> +0
+        (0x7F7FFFFF, 0x7F80),   # float32 max rounds past bf16 max to inf
+        (0x7F7F7FFF, 0x7F7F),   # stays at bf16 max
+        (0x80000000, 0x8000),   # -0.0
+        (0x7F800000, 0x7F80),   # inf
+    ]
+    enc = SG.bf16_bits(_f32([c[0] for c in cases]))
+    assert enc.dtype == np.uint16, f"bf16_bits gives {enc.dtype}"
+    for (src, dst), e in zip(cases, enc):
+        assert int(e) == dst, f"bf16_bits(0x{src:08X}) = 0x{int(e):04X}, expected 0x{dst:04X}"
+    # against torch's conversion: random magnitudes from 2^-140 to 2^120, both
+    # signs, with every other value forced onto an exact tie (low half 0x8000)
+    rng = np.random.default_rng(7)
+    n = 4096
+    x = (rng.standard_normal(n) * np.exp2(rng.integers(-140, 120, n))).astype(np.float32)
+    u = x.view(np.uint32).copy()
+    u[::2] = (u[::2] & np.uint32(0xFFFF0000)) | np.uint32(0x8000)
+    u[1::4] |= np.uint32(0x00010000)    # odd bf16 LSB under some of the ties
+    x = u.view(np.float32)
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16)
+    ref_bits = ref.view(torch.int16).numpy().view(np.uint16)
+    enc = SG.bf16_bits(x)
+    bad = np.nonzero(enc != ref_bits)[0]
+    assert bad.size == 0, f"bf16_bits differs from torch at {bad.size} values, e.g. 0x{u[bad[0]]:08X}"
+    assert np.array_equal(O.decode(ref_bits), ref.double().numpy()), "decode differs from torch bfloat16 -> float64"
+    # the round trip lands within half a bf16 unit (2^-8 relative) of the source
+    rt = O.decode(SG.bf16_bits(x))
+    fin = np.isfinite(rt) & (np.abs(x) >= 2.0 ** -126)
+    rel = np.abs(rt[fin] - x[fin]) / np.abs(x[fin].astype(np.float64))
+    assert rel.max() <= 2.0 ** -8, f"round trip relative error {rel.max():.3e}"
+
+
 ALL_CHECKS = [
+    check_bf16_codec,
     check_timestep_zero, check_timestep_frequencies, check_silu, check_gelu_tanh,
     check_linear_bruteforce, check_layer_norm, check_modulate, check_rms_norm_heads,
     check_grid_positions, check_rope, check_attention_bruteforce, check_attention_invariants,

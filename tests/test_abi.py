@@ -43,7 +43,7 @@ def test_library_exports_every_header_function():
 
 def test_abi_version_and_strings():
     L = _lib()
-    assert L.dit_abi_version() == 2
+    assert L.dit_abi_version() == 3
     assert L.dit_status_string(B.DIT_ERR_WORKSPACE) == b"workspace too small"
     assert L.dit_status_string(B.DIT_OK) == b"ok"
 
@@ -65,8 +65,10 @@ def test_attention_rejects_bad_arguments():
     bad, pbad = _cu([0, 10, 5])
     nz, pnz = _cu([1, 10])
     S = ctypes.c_void_p(0)
+    # q, k, v, o in distinct (fake) ranges, so overlap is not what fails
+    PK, PV, PO = ctypes.c_void_p(0x1000000), ctypes.c_void_p(0x2000000), ctypes.c_void_p(0x3000000)
     call = lambda q, pq, pk, n_req, H, d, scale, dt, qs=128: L.dit_attention_varlen(
-        q, P, P, P, qs, 128, 128, 128, pq, pk, n_req, H, d, scale, dt, S)
+        q, PK, PV, PO, qs, 128, 128, 128, pq, pk, n_req, H, d, scale, dt, S)
     assert call(None, pcu, pcu, 1, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
     assert b"q is NULL" in L.dit_last_error()
     assert call(P_MIS, pcu, pcu, 1, 1, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
@@ -79,8 +81,33 @@ def test_attention_rejects_bad_arguments():
     assert call(P, pcu, pcu, 1, 1, 64, 0.1, B.DIT_BF16) == B.DIT_ERR_UNSUPPORTED
     assert call(P, pcu, pcu, 1, 1, 96, 0.1, B.DIT_F32) == B.DIT_ERR_UNSUPPORTED
     assert call(P, pcu, pcu, 1, 2, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG   # stride < H*d
-    assert call(P, pcu, pcu, 1, 1, 128, 0.0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 1, 1, 128, float("inf"), B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert call(P, pcu, pcu, 1, 1, 128, float("nan"), B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
+    assert b"softmax_scale" in L.dit_last_error()
     assert call(P, pcu, pcu, 1, 1, 128, 0.1, 7) == B.DIT_ERR_INVALID_ARG
+
+
+def test_attention_rejects_output_overlapping_inputs():
+    """o is written while q, k, v are read: any shared byte is rejected on the
+    host (10 rows of stride 128 bf16 span 2,560 bytes)."""
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cu, pcu = _cu([0, 10])
+    q, k, v = 0x1000000, 0x2000000, 0x3000000
+    f = lambda o, qs=128: L.dit_attention_varlen(ctypes.c_void_p(q), ctypes.c_void_p(k), ctypes.c_void_p(v),
+                                                 ctypes.c_void_p(o), qs, 128, 128, 128, pcu, pcu, 1, 1, 128, 0.0,
+                                                 B.DIT_BF16, S)
+    assert f(q) == B.DIT_ERR_INVALID_ARG and b"o overlaps q" in L.dit_last_error()
+    assert f(k + 2560 - 16) == B.DIT_ERR_INVALID_ARG and b"o overlaps k" in L.dit_last_error()
+    assert f(v - 2560 + 16) == B.DIT_ERR_INVALID_ARG and b"o overlaps v" in L.dit_last_error()
+    # o inside q's rows (interleaved columns of one buffer) counts as overlap
+    assert f(q + 256, qs=256) == B.DIT_ERR_INVALID_ARG and b"o overlaps q" in L.dit_last_error()
+    # q, k and v may share one buffer: only o's range matters (fails later, on the work-item count)
+    cu2, pcu2 = _cu([0, 1 << 30])
+    st = L.dit_attention_varlen(ctypes.c_void_p(q), ctypes.c_void_p(q + 256), ctypes.c_void_p(q + 512),
+                                ctypes.c_void_p(1 << 46), 64 * 128 * 3, 64 * 128 * 3, 64 * 128 * 3, 64 * 128, pcu2,
+                                pcu2, 1, 64, 128, 0.0, B.DIT_BF16, S)
+    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error()
 
 
 def test_linear_rejects_bad_arguments():
@@ -265,6 +292,35 @@ def test_attention_rejects_too_many_work_items():
     numbers (2^27): rejected on the host, nothing launched."""
     L = _lib()
     cu, pcu = _cu([0, 1 << 30])
-    st = L.dit_attention_varlen(P, P, P, P, 64 * 128, 64 * 128, 64 * 128, 64 * 128, pcu, pcu, 1, 64, 128, 0.1,
-                                B.DIT_BF16, ctypes.c_void_p(0))
+    st = L.dit_attention_varlen(P, P, P, ctypes.c_void_p(1 << 46), 64 * 128, 64 * 128, 64 * 128, 64 * 128, pcu,
+                                pcu, 1, 64, 128, 0.1, B.DIT_BF16, ctypes.c_void_p(0))
     assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error()
+
+
+def test_block_seams_take_timesteps_or_modulation():
+    """Both seams take the conditioning as dit_block_forward does: t (the
+    block's timestep MLP and adaLN weights are read) or a precomputed mod
+    (those weights are not read).  Every call stops at the workspace check,
+    after the arguments it depends on have been accepted."""
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cfg, w, vl = _block_structs()
+    need = L.dit_block_workspace_size(ctypes.byref(cfg.c), ctypes.byref(vl.c))
+    pre = lambda w, t, mod: L.dit_block_pre_attention(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P, t,
+                                                       mod, P, None, need, S)
+    post = lambda w, t, mod: L.dit_block_post_attention(ctypes.byref(cfg.c), ctypes.byref(w), ctypes.byref(vl.c), P,
+                                                         P, P, t, mod, P, None, need, S)
+    assert pre(w, P, P) == B.DIT_ERR_WORKSPACE
+    assert post(w, None, P) == B.DIT_ERR_WORKSPACE
+    assert post(w, P, None) == B.DIT_ERR_WORKSPACE
+    assert post(w, None, None) == B.DIT_ERR_INVALID_ARG and b"t is NULL" in L.dit_last_error()
+    assert pre(w, None, None) == B.DIT_ERR_INVALID_ARG and b"mod is NULL" in L.dit_last_error()
+    for missing in ("w_t1", "b_t2", "w_ada"):
+        cfg, w, vl = _block_structs()
+        setattr(w, missing, None)
+        # from t: the conditioning weights are needed
+        assert pre(w, P, P) == B.DIT_ERR_INVALID_ARG and missing.encode() in L.dit_last_error()
+        assert post(w, P, None) == B.DIT_ERR_INVALID_ARG and missing.encode() in L.dit_last_error()
+        # from mod: they are not read
+        assert pre(w, None, P) == B.DIT_ERR_WORKSPACE, L.dit_last_error()
+        assert post(w, None, P) == B.DIT_ERR_WORKSPACE, L.dit_last_error()

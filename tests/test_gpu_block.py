@@ -149,3 +149,37 @@ def test_block_forward_with_precomputed_modulation():
     B.block_forward(db.cfg, B.make_weights(d2), db.vl, db.d["x"], None, db.d["txt"], y, db.ws, mod=mod)
     torch.cuda.synchronize()
     assert torch.equal(y, y_ref)
+
+
+def test_block_seams_with_precomputed_modulation():
+    """The seams take a precomputed modulation like dit_block_forward does:
+    pre(mod) -> attention -> post(mod), with the block's timestep MLP and
+    adaLN weights absent, equals forward(mod) bit for bit; post(t) (the
+    modulation computed inside) equals post(mod) bit for bit."""
+    wl = SMALL_PACKED
+    log("case seams with precomputed modulation")
+    db = DeviceBlock(wl)
+    B = db.B
+    T, D = wl.n_rows, wl.hidden
+    mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
+    B.timestep_modulation(db.cfg, db.w, db.d["t"], mod, db.ws)
+    d2 = dict(db.d)
+    for n in ("w_t1", "b_t1", "w_t2", "b_t2", "w_ada", "b_ada"):
+        d2[n] = None
+    w2 = B.make_weights(d2)
+    y_ref = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+    B.block_forward(db.cfg, w2, db.vl, db.d["x"], None, db.d["txt"], y_ref, db.ws, mod=mod)
+    mod_in = mod.clone()
+    qkv = empty((T, 3 * D), "bf16")
+    B.block_pre_attention(db.cfg, w2, db.vl, db.d["x"], None, mod_in, qkv, db.ws)
+    o = empty((T, D), "bf16")
+    cu = wl.cu_seqlens()
+    B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, wl.n_heads, wl.head_dim)
+    y = empty((T, D), "bf16")
+    B.block_post_attention(db.cfg, w2, db.vl, db.d["x"], o, db.d["txt"], mod_in, y, db.ws)
+    y_t = empty((T, D), "bf16")
+    B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], o, db.d["txt"], None, y_t, db.ws, t=db.d["t"])
+    torch.cuda.synchronize()
+    assert torch.equal(mod_in, mod), "pre_attention with t NULL wrote mod"
+    assert torch.equal(y, y_ref)
+    assert torch.equal(y_t, y_ref)

@@ -5,6 +5,7 @@ import numpy as np
 import pytest
 
 from oracle import dit_block as O
+import synth.gen as SG
 from oracle_pins import ALL_CHECKS
 
 
@@ -168,5 +169,66 @@ MUTANTS = {
 def test_mutant_is_caught(name, monkeypatch):
     fn_name, fn = MUTANTS[name]
     monkeypatch.setattr(O, fn_name, fn)
+    failed = _fails(ALL_CHECKS)
+    assert failed, f"no pin catches the mutant {name!r}"
+
+
+# ------------------------------------------------ the bf16 storage format
+# The oracle's decoding and the shared input encoder, each broken the way a
+# plausible implementation could be.
+
+
+def m_decode_shift15(a):
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(15)).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def m_decode_fp16(a):
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return a.view(np.float16).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def m_decode_float32_of_sign(a):
+    # drops the sign bit (masks with 0x7FFF)
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return ((a.astype(np.uint32) & np.uint32(0x7FFF)) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def m_bits_half_up(a):
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    return ((u + np.uint32(0x8000)) >> np.uint32(16)).astype(np.uint16)
+
+
+def m_bits_truncate(a):
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    return (u >> np.uint32(16)).astype(np.uint16)
+
+
+def m_bits_ties_odd(a):
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    return ((u + np.uint32(0x7FFF) + (np.uint32(1) - lsb)) >> np.uint32(16)).astype(np.uint16)
+
+
+CODEC_MUTANTS = {
+    "decode shifts by 15": (O, "decode", m_decode_shift15),
+    "decode reads float16": (O, "decode", m_decode_fp16),
+    "decode drops the sign": (O, "decode", m_decode_float32_of_sign),
+    "bf16_bits rounds half up": (SG, "bf16_bits", m_bits_half_up),
+    "bf16_bits truncates": (SG, "bf16_bits", m_bits_truncate),
+    "bf16_bits ties to odd": (SG, "bf16_bits", m_bits_ties_odd),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CODEC_MUTANTS))
+def test_codec_mutant_is_caught(name, monkeypatch):
+    mod, fn_name, fn = CODEC_MUTANTS[name]
+    monkeypatch.setattr(mod, fn_name, fn)
     failed = _fails(ALL_CHECKS)
     assert failed, f"no pin catches the mutant {name!r}"
