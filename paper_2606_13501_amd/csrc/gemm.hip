@@ -91,8 +91,8 @@ __device__ __forceinline__ int row_swizzle(int r) { return (r >> 1) & 7; }
 
 // Raw buffer descriptor over `bytes` bytes from `base`.  The hardware's range
 // check covers the lane offset only (not the scalar offset), so a load
-// returns zeros where its lane offset is past the end; the loads below keep
-// their scalar offsets inside the operand themselves (see piece_rmax).
+// returns zeros where its lane offset is past the end; the loads below carry
+// every row offset in the lane offset.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   const uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
@@ -144,8 +144,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   auto a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
   auto w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
   // Row 8 q + i / 8 has row_swizzle = 4 (q % 2) + i / 16, so the lane part of
-  // a load's offset takes one of two values per operand (by the parity of q)
-  // and the rest, 8 q rows, is uniform (the scalar offset of the load).
+  // a load's offset is one of two values per operand (by the parity of q)
+  // plus 8 q rows, a uniform value.
   int a_vo[2], w_vo[2];
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
@@ -153,26 +153,23 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     a_vo[par] = (lane >> 3) * (int)lda * 2 + c * 16;
     w_vo[par] = (lane >> 3) * (int)ldw * 2 + c * 16;
   }
-  // The scalar part of a load's offset is the first row of its 8-row piece.
-  // In a ragged last tile (fewer than 256 rows of A or W left) pieces past
-  // the end are moved back onto the last 8 rows, and with fewer than 8 rows
-  // left every piece starts at row 0 and the lane offsets of the missing
-  // rows fall past the descriptor's end (zeros): no load leaves the operand.
-  // The rows loaded in place of the missing ones only feed outputs that are
-  // never stored.  rmax: the largest in-bounds piece start of the tile.
-  auto piece_rmax = [](int rows_left, int tile) { return max(min(rows_left, tile) - 8, 0); };
-  int a_rmax = piece_rmax(M - m0, BM), w_rmax = piece_rmax(N - n0, BN);
-  auto a_so = [&](int u, int rmax) { return min(8 * (kLoads * wave + u), rmax) * 2 * (int)lda; };   // bytes
-  auto w_so = [&](int u, int rmax) { return min(8 * (kLoads * wave + u), rmax) * 2 * (int)ldw; };
-  // steps past the last K step (prologue loads of a short K) reload the last one
+  // A load's lane offset is its row inside the tile (piece row 8 q plus the
+  // lane's row i / 8) and its chunk; the scalar offset is the K step only.
+  // The descriptor's range check sees the whole row offset, so rows past the
+  // end of the operand (a ragged last tile) read as zeros and no load leaves
+  // the operand.  The piece part 8 q rows is uniform (a scalar added per
+  // load).  Steps past the last K step (prologue loads of a short K) reload
+  // the last one.
+  auto a_po = [&](int u) { return (kLoads * wave + u) * 16 * (int)lda; };   // 8 q rows, in bytes
+  auto w_po = [&](int u) { return (kLoads * wave + u) * 16 * (int)ldw; };
   auto k_off = [&](int step) { return min(step, K / BK - 1) * BK * 2; };
   struct Stage { u32x4 a[kLoads], w[kLoads]; };   // one step of this wave's pieces
   auto gload = [&](Stage& r, int step) {
     const int soff = k_off(step);
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      r.a[u] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[u & 1], soff + a_so(u, a_rmax), 0);
-      r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[u & 1], soff + w_so(u, w_rmax), 0);
+      r.a[u] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[u & 1] + a_po(u), soff, 0);
+      r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[u & 1] + w_po(u), soff, 0);
     }
   };
   auto sstore = [&](const Stage& r, int step) {
@@ -246,8 +243,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
       u32x4& v = u < 8 ? R.a[p] : R.w[p];
       if (do_store) *reinterpret_cast<u32x4*>(st + (u < 8 ? 0 : kTileBytes) + p * 1024) = v;
       if (do_load)
-        v = u < 8 ? __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[p & 1], soff + a_so(p, a_rmax), 0)
-                  : __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[p & 1], soff + w_so(p, w_rmax), 0);
+        v = u < 8 ? __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[p & 1] + a_po(p), soff, 0)
+                  : __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[p & 1] + w_po(p), soff, 0);
     }
   };
 
@@ -274,15 +271,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // single tile.)
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   u32x4 nad{}, nwd{};   // the next tile's A and W
-  int n_armax = 0, n_wrmax = 0;
   bool has_next = false;
   auto dma_step = [&](int step) {   // step 0 or 1 of the next tile into slot `step` (K / 64 >= 6 here)
     const uint32_t st = lds_base + step * kStageBytes + kLoads * wave * 1024;
     const int soff = step * BK * 2;
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      load_lds16(nad, a_vo[u & 1], soff + a_so(u, n_armax), st + u * 1024);
-      load_lds16(nwd, w_vo[u & 1], soff + w_so(u, n_wrmax), st + kTileBytes + u * 1024);
+      load_lds16(nad, a_vo[u & 1] + a_po(u), soff, st + u * 1024);
+      load_lds16(nwd, w_vo[u & 1] + w_po(u), soff, st + kTileBytes + u * 1024);
     }
   };
   Stage r0, r1;
@@ -326,8 +322,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
       seq.coords(it + 1, tm1, tn1);
       nad = make_desc(A + (int64_t)tm1 * BM * lda, ((int64_t)(M - tm1 * BM - 1) * lda + K) * 2);
       nwd = make_desc(W + (int64_t)tn1 * BN * ldw, ((int64_t)(N - tn1 * BN - 1) * ldw + K) * 2);
-      n_armax = piece_rmax(M - tm1 * BM, BM);
-      n_wrmax = piece_rmax(N - tn1 * BN, BN);
     }
     // r0 / r1 carry steps 2 / 3; keep the two register stages' loads in this
     // order (as in the loop), so the wait counts the compiler derives inside
@@ -479,8 +473,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     n0 = tn1 * BN;
     a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
     w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
-    a_rmax = n_armax;
-    w_rmax = n_wrmax;
   }
 }
 

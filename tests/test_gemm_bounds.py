@@ -3,43 +3,47 @@ byte a load touches lies inside the operand, for ragged and exact tiles.
 
 The kernel forms each 16-byte load from a buffer descriptor (base = first
 row of the tile, range = bytes up to the end of the operand's last row), a
-lane offset (row inside an 8-row piece and a swizzled 16-byte chunk) and a
-scalar offset (the piece's first row, clamped to the last in-bounds piece,
-plus the K step).  The hardware zero-fills a load whose lane offset is past
-the range and does not range-check the scalar offset, so the scalar part
-alone must keep every load inside the operand.  This model recomputes those
-offsets the same way for every tile row, wave, piece, lane and K step."""
+lane offset (the row inside the tile, 8 q + i / 8 for piece q and lane i,
+and a swizzled 16-byte chunk) and a scalar offset (the K step).  The
+hardware zero-fills a load whose lane offset is past the range and does not
+range-check the scalar offset, so the rows past a ragged tile's end must be
+caught by the lane offset and the K step must stay inside a row.  This model
+recomputes those offsets the same way for every tile row, wave, piece, lane
+and K step."""
 import numpy as np
 import pytest
 
 BM, BK, WAVES, LOADS = 256, 64, 4, 8
 
 
-def load_extents(M, K, ld, ragged_rows=None):
+def load_extents(M, K, ld, row_in_lane=True):
     """(lowest, highest) byte touched by the loads of every tile, relative to
-    the operand's base, for all K steps the kernel issues (0 .. max(K/64, 4))."""
+    the operand's base, for all K steps the kernel issues (0 .. max(K/64, 4)).
+    row_in_lane=False models the earlier layout (piece row in the scalar
+    offset, outside the range check)."""
     tiles = (M + BM - 1) // BM
     kt = K // BK
     lane = np.arange(64)
     lo, hi = np.inf, -np.inf
+    # the prologue issues steps 0..3, the loop steps up to K/64 - 1; a step
+    # past the last one reloads the last one
+    steps = np.minimum(np.arange(max(kt, 4)), kt - 1) * BK * 2
     for tm in range(tiles):
         m0 = tm * BM
         n_rec = ((M - m0 - 1) * ld + K) * 2
-        rmax = max(min(M - m0, BM) - 8, 0)
         for wave in range(WAVES):
             for u in range(LOADS):
                 q = LOADS * wave + u
-                par = q & 1
-                c = (lane & 7) ^ (4 * par + (lane >> 4))
-                vo = (lane >> 3) * ld * 2 + c * 16
+                c = (lane & 7) ^ (4 * (q & 1) + (lane >> 4))
+                lane_part = (lane >> 3) * ld * 2 + c * 16
+                piece = 8 * q * ld * 2
+                vo = lane_part + piece if row_in_lane else lane_part
                 live = vo < n_rec                       # otherwise zero-filled, nothing read
                 if not live.any():
                     continue
-                # the prologue issues steps 0..3, the loop steps up to K/64 - 1
-                steps = np.minimum(np.arange(max(kt, 4)), kt - 1) * BK * 2
-                base = m0 * ld * 2 + min(8 * q, rmax) * 2 * ld
-                lo = min(lo, base + vo[live].min() + steps.min())
-                hi = max(hi, base + vo[live].max() + steps.max() + 15)
+                addr = m0 * ld * 2 + vo[live] + (0 if row_in_lane else piece)
+                lo = min(lo, addr.min() + steps.min())
+                hi = max(hi, addr.max() + steps.max() + 15)
     return lo, hi
 
 
@@ -59,10 +63,9 @@ def test_gemm_loads_stay_inside_operand(M, K, ld):
     assert hi <= last, f"a load reaches byte {hi}, past the operand's last byte {last}"
 
 
-def test_unclamped_offsets_would_leave_the_operand():
-    """Without the clamp (scalar offset = 8 q rows) the 720p ragged tile reads
-    past the end: what the clamp is there for."""
+def test_scalar_piece_offset_would_leave_the_operand():
+    """With the piece row in the (unchecked) scalar offset, the 720p ragged
+    tile reads past the operand's end: what the lane-offset layout prevents."""
     M, K, ld = 75600, 5120, 5120
-    m0 = (M // BM) * BM
-    worst = m0 * ld * 2 + (8 * (LOADS * WAVES - 1) + 7) * ld * 2 + (K - 1) * 2
-    assert worst > ((M - 1) * ld + K) * 2 - 1
+    lo, hi = load_extents(M, K, ld, row_in_lane=False)
+    assert hi > ((M - 1) * ld + K) * 2 - 1
