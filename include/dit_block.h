@@ -16,7 +16,8 @@
  * Conventions shared by every entry point:
  *  - Every pointer not marked "host" is device memory on the current HIP
  *    device.  The caller owns all memory; the library allocates and frees
- *    nothing and keeps no mutable global state, so calls are thread-safe.
+ *    nothing and keeps no mutable global state, so calls are thread-safe
+ *    (the one exception, dit_timestep_modulation_noalloc, says so).
  *  - Tensors are row-major.  Activations are token-major [rows, width];
  *    Linear weights are [out, in] (every GEMM is A . W^T); vectors are dense.
  *  - dtype DIT_BF16: activations, weights, norm gains and biases are bfloat16;
@@ -164,6 +165,23 @@ dit_status dit_block_post_attention(const dit_block_config *cfg, const dit_block
 dit_status dit_timestep_modulation(const dit_block_config *cfg, const dit_block_weights *w,
                                    int n_req, const float *t, float *mod, void *ws,
                                    size_t ws_bytes, hipStream_t stream);
+
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation:
+ * dit_timestep_modulation with the same arguments and results but no
+ * workspace.  Its scratch (the sinusoidal encoding and the timestep MLP's two
+ * hidden vectors, (F + 2D) * n_req floats, each part 256-byte aligned) lives
+ * in a static device array of DIT_NOALLOC_SCRATCH_BYTES bytes that every GPU
+ * the library runs on holds until the process ends; the library looks up its
+ * address once per device, on the first call there.  Nothing is allocated or
+ * freed.  A size over the array gives DIT_ERR_UNSUPPORTED (nothing launched).
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind (each call writes all it reads, so nothing needs clearing); calls
+ * that overlap on one GPU (other streams or threads) race on it. */
+#define DIT_NOALLOC_SCRATCH_BYTES (8u << 20)
+dit_status dit_timestep_modulation_noalloc(const dit_block_config *cfg, const dit_block_weights *w,
+                                           int n_req, const float *t, float *mod,
+                                           hipStream_t stream);
 
 /* Scaled dot-product attention over a packed batch, non-causal, no mask:
  * for request r and head h, O = softmax(Q K^T * softmax_scale) V with queries

@@ -7,6 +7,6 @@ it every entry point raises ``binding.ExtensionMissing``.
 from . import binding  # noqa: F401
 from .binding import (  # noqa: F401
     BlockConfig, Varlen, DitError, ExtensionMissing, make_weights, block_workspace_size,
-    block_forward, block_pre_attention, block_post_attention, timestep_modulation,
+    block_forward, block_pre_attention, block_post_attention, timestep_modulation, timestep_modulation_noalloc,
     attention_varlen, adaln_modulate, layer_norm_affine, linear, qk_norm_rope, gated_residual,
 )

@@ -136,6 +136,7 @@ def lib() -> ctypes.CDLL:
         "dit_block_pre_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, sz, vp]),
         "dit_block_post_attention": (i32, [PC, PW, PV, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "dit_timestep_modulation": (i32, [PC, PW, i32, vp, vp, vp, sz, vp]),
+        "dit_timestep_modulation_noalloc": (i32, [PC, PW, i32, vp, vp, vp]),
         "dit_attention_varlen": (i32, [vp, vp, vp, vp, i64, i64, i64, i64, PI, PI, i32, i32, i32, f32, i32, vp]),
         "dit_adaln_modulate": (i32, [vp, vp, vp, i64, PI, i32, i32, f32, vp, i32, vp]),
         "dit_layer_norm_affine": (i32, [vp, vp, vp, i64, i32, f32, vp, i32, vp]),
@@ -167,7 +168,8 @@ def lib() -> ctypes.CDLL:
 
 def exported_symbols() -> Sequence[str]:
     return [n for n in ("dit_block_workspace_size", "dit_block_forward", "dit_block_pre_attention",
-                        "dit_block_post_attention", "dit_timestep_modulation", "dit_attention_varlen",
+                        "dit_block_post_attention", "dit_timestep_modulation",
+                        "dit_timestep_modulation_noalloc", "dit_attention_varlen",
                         "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
                         "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
@@ -284,6 +286,13 @@ def timestep_modulation(cfg, weights, t, mod, ws, stream=None):
     _check(lib().dit_timestep_modulation(ctypes.byref(cfg.c), ctypes.byref(weights), int(t.numel()), _ptr(t),
                                          _ptr(mod), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "dit_timestep_modulation")
+
+
+def timestep_modulation_noalloc(cfg, weights, t, mod, stream=None):
+    """dit_timestep_modulation without a workspace (the library's static scratch)."""
+    _check(lib().dit_timestep_modulation_noalloc(ctypes.byref(cfg.c), ctypes.byref(weights), int(t.numel()),
+                                                 _ptr(t), _ptr(mod), _stream(stream)),
+           "dit_timestep_modulation_noalloc")
 
 
 def attention_varlen(q, k, v, o, cu_q, cu_k, n_heads, head_dim, softmax_scale=None, stream=None):

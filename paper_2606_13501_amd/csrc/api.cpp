@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "dit_block.h"
@@ -528,6 +529,63 @@ dit_status run_cond_parts(const dit_block_config* c, int n_req, const float* t, 
 
 }  // namespace
 
+// Scratch of dit_timestep_modulation_noalloc: one array per GPU, held until
+// the process ends.  Host code never uses the name `scratch` as an address
+// (on the host it is a stand-in, not device memory); it uses the device
+// address looked up with hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[DIT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device, with that device current).
+dit_status scratch_address(void** out) {
+  int dev = -1;
+  DIT_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(DIT_ERR_UNSUPPORTED, "device %d (at most %d devices)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    DIT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(DIT_ERR_HIP, "hipGetSymbolAddress(scratch) gave NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DIT_OK;
+}
+
+// Checks shared by both conditioning entry points; the scratch layout is
+// e [R,F], a1 [R,D], c [R,D], each 256-byte aligned.
+dit_status check_modulation_call(const dit_block_config* cfg, const dit_block_weights* w, int n_req, const float* t,
+                                 float* mod) {
+  DIT_TRY(check_cfg(cfg));
+  DIT_TRY(check_cond_weights(w));
+  if (n_req < 1 || n_req > DIT_MAX_REQ) return fail(DIT_ERR_INVALID_ARG, "n_req = %d outside 1..%d", n_req, DIT_MAX_REQ);
+  DIT_TRY(check_ptr(t, "t"));
+  DIT_TRY(check_ptr(mod, "mod"));
+  return DIT_OK;
+}
+
+size_t modulation_scratch_bytes(const dit_block_config* cfg, int n_req) {
+  return round256((size_t)cfg->freq_dim * n_req * 4) + 2 * round256((size_t)cfg->hidden * n_req * 4);
+}
+
+dit_status run_modulation(const dit_block_config* cfg, const dit_block_weights* w, int n_req, const float* t,
+                          float* mod, char* p, hipStream_t stream) {
+  float* e = (float*)p;
+  p += round256((size_t)cfg->freq_dim * n_req * 4);
+  float* a1 = (float*)p;
+  p += round256((size_t)cfg->hidden * n_req * 4);
+  float* cc = (float*)p;
+  return run_cond(cfg, w, n_req, t, mod, e, a1, cc, stream);
+}
+
+}  // namespace
+
 namespace dit {
 // Sets this thread's dit_last_error() message (used by the other C-ABI units).
 void set_last_error(const std::string& msg) { g_last_error = msg; }
@@ -623,21 +681,24 @@ dit_status dit_block_post_attention(const dit_block_config* cfg, const dit_block
 dit_status dit_timestep_modulation(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
                                    const float* t, float* mod, void* ws, size_t ws_bytes, hipStream_t stream) {
   g_last_error.clear();
-  DIT_TRY(check_cfg(cfg));
-  DIT_TRY(check_cond_weights(w));
-  if (n_req < 1 || n_req > DIT_MAX_REQ) return fail(DIT_ERR_INVALID_ARG, "n_req = %d outside 1..%d", n_req, DIT_MAX_REQ);
-  DIT_TRY(check_ptr(t, "t"));
-  DIT_TRY(check_ptr(mod, "mod"));
-  const size_t need = (size_t)(cfg->freq_dim + 2 * cfg->hidden) * n_req * 4 + 3 * 256;
+  DIT_TRY(check_modulation_call(cfg, w, n_req, t, mod));
+  const size_t need = modulation_scratch_bytes(cfg, n_req);
   if (!ws || ((uintptr_t)ws & 255u)) return fail(DIT_ERR_WORKSPACE, "workspace NULL or not 256-byte aligned");
   if (ws_bytes < need) return fail(DIT_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
-  char* p = (char*)ws;
-  float* e = (float*)p;
-  p += round256((size_t)cfg->freq_dim * n_req * 4);
-  float* a1 = (float*)p;
-  p += round256((size_t)cfg->hidden * n_req * 4);
-  float* cc = (float*)p;
-  return run_cond(cfg, w, n_req, t, mod, e, a1, cc, stream);
+  return run_modulation(cfg, w, n_req, t, mod, (char*)ws, stream);
+}
+
+dit_status dit_timestep_modulation_noalloc(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
+                                           const float* t, float* mod, hipStream_t stream) {
+  g_last_error.clear();
+  DIT_TRY(check_modulation_call(cfg, w, n_req, t, mod));
+  const size_t need = modulation_scratch_bytes(cfg, n_req);
+  if (need > DIT_NOALLOC_SCRATCH_BYTES)
+    return fail(DIT_ERR_UNSUPPORTED, "scratch of %zu bytes needed, the static array holds %zu", need,
+                (size_t)DIT_NOALLOC_SCRATCH_BYTES);
+  void* p = nullptr;
+  DIT_TRY(scratch_address(&p));
+  return run_modulation(cfg, w, n_req, t, mod, (char*)p, stream);
 }
 
 dit_status dit_attention_varlen(const void* q, const void* k, const void* v, void* o, int64_t q_row_stride,

@@ -324,3 +324,22 @@ def test_block_seams_take_timesteps_or_modulation():
         # from mod: they are not read
         assert pre(w, None, P) == B.DIT_ERR_WORKSPACE, L.dit_last_error()
         assert post(w, None, P) == B.DIT_ERR_WORKSPACE, L.dit_last_error()
+
+
+def test_noalloc_modulation_rejects_before_any_device_call():
+    """The no-workspace conditioning validates like dit_timestep_modulation and
+    rejects a scratch need over its static array on the host."""
+    L = _lib()
+    S = ctypes.c_void_p(0)
+    cfg, w, _ = _block_structs()
+    f = lambda cfg, n, t=P, mod=P: L.dit_timestep_modulation_noalloc(ctypes.byref(cfg.c), ctypes.byref(w), n, t, mod, S)
+    assert f(cfg, 0) == B.DIT_ERR_INVALID_ARG
+    assert f(cfg, 65) == B.DIT_ERR_INVALID_ARG
+    assert f(cfg, 1, t=None) == B.DIT_ERR_INVALID_ARG and b"t is NULL" in L.dit_last_error()
+    assert f(cfg, 1, mod=P_MIS) == B.DIT_ERR_INVALID_ARG
+    w.w_ada = None
+    assert f(cfg, 1) == B.DIT_ERR_INVALID_ARG and b"w_ada" in L.dit_last_error()
+    w.w_ada = P.value
+    # F = 32768, D = 8192, 64 requests: (F + 2D) * 64 * 4 = 12 MiB > 8 MiB
+    big = B.BlockConfig(8192, 64, 128, 8192, 32768, (0, 64, 64), B.DIT_BF16)
+    assert f(big, 64) == B.DIT_ERR_UNSUPPORTED and b"static array" in L.dit_last_error()
