@@ -294,10 +294,12 @@ dit_status run_norm_rope(void* q, void* k, int64_t stride, int64_t n_rows, int n
 
 dit_status run_attention(const void* q, const void* k, const void* v, void* o, int64_t qs, int64_t ks,
                          int64_t vs, int64_t os, const ReqTable& cq, const ReqTable& ck, int n_heads,
-                         int head_dim, float scale, dit_dtype dt, hipStream_t s) {
+                         int head_dim, float scale, dit_dtype dt, hipStream_t s, const void* q_gain = nullptr,
+                         float q_eps = 0.f) {
   AttnArgs p;
   p.q = q; p.k = k; p.v = v; p.o = o; p.q_stride = qs; p.k_stride = ks; p.v_stride = vs; p.o_stride = os;
   p.cq = cq; p.ck = ck; p.n_heads = n_heads; p.head_dim = head_dim; p.scale = scale; p.dtype = dt;
+  p.q_gain = q_gain; p.q_eps = q_eps;
   return hip_status(launch_attention(p, s), "attention");
 }
 
@@ -363,7 +365,9 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   DIT_TRY(run_ln_affine(ws.x1, w->g_ca, w->b_ca, T, D, c->ln_eps, ws.h, dt, s));
   DIT_TRY(run_linear(ws.h, D, w->w_cq, D, w->b_cq, ws.cq, D, T, D, D, DIT_EPI_NONE, nullptr, 0, nullptr, 0, req, dt,
                      s, "cross query projection"));
-  if (c->qk_norm) {
+  // bf16: the RMSNorm of cq happens as the cross-attention loads it
+  const bool cq_norm_in_attn = c->qk_norm && dt == DIT_BF16;
+  if (c->qk_norm && !cq_norm_in_attn) {
     const int zero[3] = {0, 0, 0};
     DIT_TRY(run_norm_rope(ws.cq, nullptr, D, T, c->n_heads, c->head_dim, w->g_cq, nullptr, c->rms_eps, zero, 0.f,
                           nullptr, dt, s));
@@ -376,7 +380,8 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   }
   // oc = cross attention (queries: the request's latent rows, keys: its text rows)
   DIT_TRY(run_attention(ws.cq, ckv, ckv + D * es, ws.o, D, 2 * D, 2 * D, D, req, req_txt, c->n_heads,
-                        c->head_dim, 1.0f / sqrtf((float)c->head_dim), dt, s));
+                        c->head_dim, 1.0f / sqrtf((float)c->head_dim), dt, s,
+                        cq_norm_in_attn ? w->g_cq : nullptr, c->rms_eps));
   // x2 = x1 + (oc W_co^T + b_co), in place in x1
   DIT_TRY(run_linear(ws.o, D, w->w_co, D, w->b_co, ws.x1, D, T, D, D, DIT_EPI_RESIDUAL, ws.x1, D, nullptr, 0, req,
                      dt, s, "cross output projection"));
@@ -389,13 +394,14 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   return DIT_OK;
 }
 
-// The bf16 attention numbers its work items (256-query tiles x heads) in int
-// and splits them over the XCDs with products that must stay below 2^31.
+// The bf16 attention numbers its work items (128- or 256-query tiles x
+// heads) in int and splits them over the XCDs with products that must stay
+// below 2^31: at most 2^26 256-query tiles (so 2^27 of 128 queries).
 dit_status check_attn_items(const int32_t* cu, int n_req, int n_heads) {
   int64_t items = 0;
   for (int r = 0; r < n_req; ++r) items += (int64_t)(cu[r + 1] - cu[r] + 255) / 256 * n_heads;
-  if (items > (1 << 27))
-    return fail(DIT_ERR_UNSUPPORTED, "attention of %lld work items (at most 2^27 query tiles x heads)",
+  if (items > (1 << 26))
+    return fail(DIT_ERR_UNSUPPORTED, "attention of %lld work items (at most 2^26 256-query tiles x heads)",
                 (long long)items);
   return DIT_OK;
 }

@@ -43,16 +43,19 @@ namespace dit {
 namespace {
 
 constexpr int D = 128;                 // head_dim of the bf16 kernel
-constexpr int BQ = 256;                // query rows per workgroup
 constexpr int BKV = 64;                // keys per tile
-constexpr int kWaves = 8;
-constexpr int kThreads = kWaves * 64;
-constexpr int kRing = 4;               // LDS ring of K/V tiles
 constexpr int kTileBytes = BKV * D * 2;          // one K or V tile (16 KiB)
 constexpr int kSlotBytes = 2 * kTileBytes;       // K tile + V tile
-constexpr int kPieces = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave and operand (2)
-constexpr int kLoadsPerTile = 2 * kPieces;       // this wave's loads of one tile
 constexpr int kXcds = 8;
+// Two shapes of the bf16 kernel, both with 32 query rows per wave:
+//  - long key ranges: 8 waves (256 query rows) per workgroup, one workgroup
+//    per compute unit, an LDS ring of 4 K/V tiles issued 3 ahead;
+//  - short key ranges (cross-attention to text, short requests): 4 waves
+//    (128 query rows), two workgroups per compute unit, a ring of 2 tiles
+//    issued 2 ahead.  A work item is then only a few tiles long, and the
+//    second workgroup's tiles keep the matrix cores busy while one workgroup
+//    loads its queries and first tiles or stores its output.
+constexpr int kShortKeys = 1024;       // longest key range that takes the short shape
 constexpr float kHeadroom = 64.0f;   // log2 units; probabilities stay below 2^64
 
 struct AttnWork {
@@ -110,12 +113,20 @@ __device__ __forceinline__ void score_guard(f32x16& d) { asm volatile("s_nop 7\n
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-__global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
+// QNORM: q is RMS-normalised per head (gain q_gain, epsilon q_eps) as it is
+// loaded, before the softmax scale is applied.
+template <int WAVES, int RING, bool QNORM>
+__global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O, int64_t qs, int64_t ks, int64_t vs, int64_t os, int n_heads,
-    float scale_log2, AttnWork work) {
-  // slot t % kRing holds K(t) (first 16 KiB) and V(t)
-  __shared__ __attribute__((aligned(1024))) char smem[kRing * kSlotBytes];
+    float scale_log2, const bf16* __restrict__ q_gain, float q_eps, AttnWork work) {
+  static_assert((WAVES == 8 && RING == 4) || (WAVES == 4 && RING == 2), "two shapes");
+  constexpr int BQ = 32 * WAVES;                          // query rows per workgroup
+  constexpr int kPieces = kTileBytes / 1024 / WAVES;      // 1 KiB loads per wave and operand
+  constexpr int kLoadsPerTile = 2 * kPieces;              // this wave's loads of one tile
+  constexpr int kAhead = RING == 4 ? 3 : 2;               // tiles issued ahead of the one computed
+  // slot t % RING holds K(t) (first 16 KiB) and V(t)
+  __shared__ __attribute__((aligned(1024))) char smem[RING * kSlotBytes];
   __shared__ int redo_flag[2];   // one flag per pass that may ask for another
 
   // ---- work item.  Workgroups are dispatched to the XCDs round-robin, so
@@ -155,18 +166,39 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
   // relative error of at most 2^-9 per element, the size of q's own rounding)
   const int my_q = q0 + 32 * wave + fr;
   bf16x8 qf[8];
+  bf16x8 gf[QNORM ? 8 : 1];
   {
     const bf16* qp = Q + (int64_t)min(my_q, q_end - 1) * qs + head * D + 8 * fh;
 #pragma unroll
     for (int kc = 0; kc < 8; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(qp + 16 * kc);
+    if constexpr (QNORM) {
+#pragma unroll
+      for (int kc = 0; kc < 8; ++kc) gf[kc] = *reinterpret_cast<const bf16x8*>(q_gain + 8 * fh + 16 * kc);
+    }
   }
   // the Q loads complete here, before any tile load is issued (otherwise the
   // compiler's wait for them would also wait for the tile loads)
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  typedef float f32x8 __attribute__((ext_vector_type(8)));
+  float q_mul = scale_log2;
+  if constexpr (QNORM) {
+    // RMSNorm over the head: this lane holds 64 of its 128 values, the lane
+    // 32 apart the other 64
+    float ss = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc) {
+      const f32x8 f = __builtin_convertvector(qf[kc], f32x8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(f[e], f[e], ss);
+    }
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
+    const float tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    q_mul = scale_log2 * rsqrtf(tot * (1.0f / D) + q_eps);
+  }
 #pragma unroll
   for (int kc = 0; kc < 8; ++kc) {
-    typedef float f32x8 __attribute__((ext_vector_type(8)));
-    const f32x8 f = __builtin_convertvector(qf[kc], f32x8) * scale_log2;
+    f32x8 f = __builtin_convertvector(qf[kc], f32x8) * q_mul;
+    if constexpr (QNORM) f *= __builtin_convertvector(gf[QNORM ? kc : 0], f32x8);
     qf[kc] = __builtin_convertvector(f, bf16x8);
   }
 
@@ -192,7 +224,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     const int kb = t * BKV;
     const u32x4 kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
     const u32x4 vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
-    const uint32_t st = lds_base + (uint32_t)((t % kRing) * kSlotBytes) + kPieces * wave * 1024;
+    const uint32_t st = lds_base + (uint32_t)((t % RING) * kSlotBytes) + kPieces * wave * 1024;
 #pragma unroll
     for (int u = 0; u < kPieces; ++u) {
       load_lds16(kd, k_voff[u], st + u * 1024);
@@ -236,7 +268,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
 
   // S(t) for both 32-key halves (two independent chains); FIRST: from zero
   auto S = [&](int t, auto first) __attribute__((always_inline)) {
-    const int so = (t % kRing) * kSlotBytes + k_lane;
+    const int so = (t % RING) * kSlotBytes + k_lane;
     bf16x8 ka[8], kb[8];
     ka[0] = *reinterpret_cast<const bf16x8*>(smem + so);
     kb[0] = *reinterpret_cast<const bf16x8*>(smem + so + 32 * 256);
@@ -303,7 +335,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
       }
   };
   auto PV = [&](int t) __attribute__((always_inline)) {
-    const int so = (t % kRing) * kSlotBytes;
+    const int so = (t % RING) * kSlotBytes;
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc)
 #pragma unroll
@@ -316,17 +348,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
       }
   };
   // One step: S(t), P(t), O += V(t) P(t); then tile t + 1 must be in LDS for
-  // every wave (a wave's loads of tile t + 2 may stay in flight), and tile
-  // t + 3 goes into the slot of tile t - 1, which every wave has finished.
+  // every wave.  Ring of 4: a wave's loads of tile t + 2 may stay in flight,
+  // and tile t + 3 goes into the slot of tile t - 1, which every wave has
+  // finished.  Ring of 2: tile t + 1 is the only one in flight, and tile
+  // t + 2 goes into the slot of tile t, which every wave has just finished.
   auto step = [&](int t, auto first, auto last, auto track) __attribute__((always_inline)) {
     S(t, first);
     softmax(t, first, last, track);
     PV(t);
     if (!decltype(last)::value) {
-      if (t + 2 < n_tiles) wait_vmcnt<kLoadsPerTile>();
+      if (RING == 4 && t + 2 < n_tiles) wait_vmcnt<kLoadsPerTile>();
       else wait_vmcnt<0>();
       __syncthreads();
-      if (t + 3 < n_tiles) issue(t + 3);
+      if (t + kAhead < n_tiles) issue(t + kAhead);
     }
   };
   using kOn = std::true_type;
@@ -336,7 +370,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
     for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
     l_run[0] = l_run[1] = l_run[2] = l_run[3] = 0.f;
     x_max = -INFINITY;
-    const int n_pre = min(3, n_tiles);
+    const int n_pre = min(kAhead, n_tiles);
     for (int t = 0; t < n_pre; ++t) issue(t);
     // tile 0 in LDS
     if (n_pre == 3) wait_vmcnt<2 * kLoadsPerTile>();
@@ -349,8 +383,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_bf16(
       step(0, kOn{}, kOff{}, track);
       // no compiler-tracked load may still be pending when the loop starts:
       // its tracking would otherwise put a vmcnt wait (which also waits for
-      // the tile loads in flight) at the top of every iteration
-      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
+      // the tile loads in flight) at the top of every iteration.  (The short
+      // shape's items are a few tiles long: there this wait would cost a
+      // tile's load latency per item.)
+      if constexpr (RING == 4) __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
       for (int t = 1; t + 1 < n_tiles; ++t) step(t, kOff{}, kOff{}, track);
       step(n_tiles - 1, kOff{}, kOn{}, track);
     }
@@ -481,17 +517,22 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
     return hipGetLastError();
   }
   // requests with queries, longest key range first (their tiles do the most work)
-  AttnWork w{};
   int order[DIT_MAX_REQ];
-  int n = 0;
+  int n = 0, max_k = 0;
   for (int r = 0; r < n_req; ++r)
-    if (p.cq.cu[r + 1] > p.cq.cu[r]) order[n++] = r;
+    if (p.cq.cu[r + 1] > p.cq.cu[r]) {
+      order[n++] = r;
+      max_k = max(max_k, p.ck.cu[r + 1] - p.ck.cu[r]);
+    }
   for (int i = 1; i < n; ++i) {
     int x = order[i], j = i - 1;
     int lx = p.ck.cu[x + 1] - p.ck.cu[x];
     while (j >= 0 && (p.ck.cu[order[j] + 1] - p.ck.cu[order[j]]) < lx) { order[j + 1] = order[j]; --j; }
     order[j + 1] = x;
   }
+  const bool short_keys = max_k <= kShortKeys;
+  const int bq = short_keys ? 128 : 256;
+  AttnWork w{};
   w.n_req = n;
   w.prefix[0] = 0;
   for (int i = 0; i < n; ++i) {
@@ -500,12 +541,12 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
     w.q_len[i] = p.cq.cu[r + 1] - p.cq.cu[r];
     w.k_start[i] = p.ck.cu[r];
     w.k_len[i] = p.ck.cu[r + 1] - p.ck.cu[r];
-    w.tiles_q[i] = (w.q_len[i] + BQ - 1) / BQ;
+    w.tiles_q[i] = (w.q_len[i] + bq - 1) / bq;
     w.prefix[i + 1] = w.prefix[i] + w.tiles_q[i] * p.n_heads;
   }
   const int items = w.prefix[n];
   if (items == 0) return hipSuccess;
-  if (items > (1 << 27)) return hipErrorInvalidValue;   // keeps xcd * n_r in range
+  if (items > (1 << 27)) return hipErrorInvalidValue;   // keeps (xcd + 1) * n_r in range
   // each XCD's share of every request (see the kernel); the grid covers the largest
   int per_xcd = 0;
   for (int x = 0; x < kXcds; ++x) {
@@ -518,9 +559,18 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
   }
   const int grid = per_xcd * kXcds;
   const float scale_log2 = p.scale * 1.4426950408889634f;
-  attn_fwd_bf16<<<grid, kThreads, 0, s>>>((const bf16*)p.q, (const bf16*)p.k, (const bf16*)p.v,
-                                          (bf16*)p.o, p.q_stride, p.k_stride, p.v_stride, p.o_stride,
-                                          p.n_heads, scale_log2, w);
+  const bf16* g = (const bf16*)p.q_gain;
+#define DIT_ATTN_ARGS                                                                                          \
+  (const bf16*)p.q, (const bf16*)p.k, (const bf16*)p.v, (bf16*)p.o, p.q_stride, p.k_stride, p.v_stride,        \
+      p.o_stride, p.n_heads, scale_log2, g, p.q_eps, w
+  if (short_keys) {
+    if (g) attn_fwd_bf16<4, 2, true><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
+    else attn_fwd_bf16<4, 2, false><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
+  } else {
+    if (g) attn_fwd_bf16<8, 4, true><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
+    else attn_fwd_bf16<8, 4, false><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
+  }
+#undef DIT_ATTN_ARGS
   return hipGetLastError();
 }
 

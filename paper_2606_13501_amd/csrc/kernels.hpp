@@ -32,6 +32,10 @@ struct AttnArgs {
   int n_heads, head_dim;
   float scale;
   dit_dtype dtype;
+  // bf16 only: per-head RMSNorm of q with this gain [head_dim] as q is loaded
+  // (NULL: q used as stored)
+  const void* q_gain = nullptr;
+  float q_eps = 0.f;
 };
 hipError_t launch_attention(const AttnArgs& p, hipStream_t s);
 

@@ -164,9 +164,11 @@ def generate_attention_inputs(wl: Workload, threads: Optional[int] = None) -> Di
 
 
 def generate_sampled_rows(wl: Workload, n_per_req: int, sample_id: int = 0,
-                          attn: bool = False) -> np.ndarray:
+                          attn: bool = False, tile: Optional[int] = None) -> np.ndarray:
     """Sorted global row indices: a seeded sample of each request's rows that
-    always includes the first and last row and rows at frame boundaries."""
+    always includes the first and last row and rows at frame boundaries, and
+    with ``tile`` also the first and last row of every ``tile``-row block of
+    the packed batch (global row index) that the request touches."""
     rng = np.random.default_rng([SEED, wl.wid, 1000 + sample_id])
     cu = wl.cu_attn() if attn else wl.cu_seqlens()
     out = []
@@ -179,6 +181,11 @@ def generate_sampled_rows(wl: Workload, n_per_req: int, sample_id: int = 0,
             if f * frame < n:
                 must.add(f * frame - 1)
                 must.add(f * frame)
+        if tile:
+            for g in range(cu[r] // tile * tile, cu[r + 1], tile):
+                for row in (g, g + tile - 1):
+                    if cu[r] <= row < cu[r + 1]:
+                        must.add(row - cu[r])
         must = sorted(must)[: max(2, n_per_req // 2)]
         k = max(0, min(n, n_per_req) - len(must))
         pool = np.setdiff1d(np.arange(n), np.array(must))

@@ -22,7 +22,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 import synth  # noqa: E402
 from oracle import dit_block as O  # noqa: E402
 
-N_ROWS = 32
+N_ROWS = 256
 
 
 def make(name: str) -> str:

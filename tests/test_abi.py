@@ -107,7 +107,7 @@ def test_attention_rejects_output_overlapping_inputs():
     st = L.dit_attention_varlen(ctypes.c_void_p(q), ctypes.c_void_p(q + 256), ctypes.c_void_p(q + 512),
                                 ctypes.c_void_p(1 << 46), 64 * 128 * 3, 64 * 128 * 3, 64 * 128 * 3, 64 * 128, pcu2,
                                 pcu2, 1, 64, 128, 0.0, B.DIT_BF16, S)
-    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error()
+    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error(), L.dit_last_error()
 
 
 def test_linear_rejects_bad_arguments():
@@ -294,7 +294,7 @@ def test_attention_rejects_too_many_work_items():
     cu, pcu = _cu([0, 1 << 30])
     st = L.dit_attention_varlen(P, P, P, ctypes.c_void_p(1 << 46), 64 * 128, 64 * 128, 64 * 128, 64 * 128, pcu,
                                 pcu, 1, 64, 128, 0.1, B.DIT_BF16, ctypes.c_void_p(0))
-    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error()
+    assert st == B.DIT_ERR_UNSUPPORTED and b"work items" in L.dit_last_error(), L.dit_last_error()
 
 
 def test_block_seams_take_timesteps_or_modulation():

@@ -2,12 +2,14 @@
 tokens) and the packed sequence-parallel share (four requests, 5 attention
 heads over 121,672 rows), in the launch configuration the benchmark times.
 
-The GPU computes every row; the oracle computes a seeded sample of rows
-(first and last row of every request, frame boundaries, random rows: 2048
-per request for self-attention, 256 for the per-row stages around it) from
-the same inputs.  Self-attention stages use seeded q, k, v; the whole block is
-compared with expected rows written by tests/golden/make_block_golden.py.
-The memory-bound stages are compared on every row."""
+The GPU computes every row; the oracle computes a seeded sample of 2048
+rows per request (all rows of a shorter request): the first and last row of
+every request, its frame boundaries, the first and last row of every
+256-row GEMM tile, and random rows.  Self-attention uses seeded q, k, v; the
+stages before and after it (S1-S3, S5-S12) are checked on those rows with a
+seeded attention output; the whole block is compared with expected rows
+written by tests/golden/make_block_golden.py (oracle only).  The
+memory-bound stages are compared on every row."""
 import os
 
 import numpy as np
@@ -50,7 +52,7 @@ def test_self_attention_full_size(name):
     check(g, ref, "bf16", f"{name} self-attention ({len(rows)} sampled rows)")
 
 
-@pytest.mark.parametrize("name", ["video_720p", "packed_sp8_share"])
+@pytest.mark.parametrize("name", ["video_720p", "video_480p", "packed_sp8_share"])
 def test_pre_post_attention_full_size(name):
     wl = synth.get_workload(name)
     log(f"case full-size pre/post attention {name}: rows {wl.n_rows}")
@@ -64,7 +66,8 @@ def test_pre_post_attention_full_size(name):
     y = empty((T, D), "bf16")
     B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], dev(o_in), db.d["txt"], mod, y, db.ws)
     torch.cuda.synchronize()
-    rows = synth.generate_sampled_rows(wl, 256, sample_id=4)
+    rows = synth.generate_sampled_rows(wl, 2048, sample_id=4, tile=256)
+    log(f"  {len(rows)} sampled rows (every 256-row tile's first and last row among them)")
     idx = torch.from_numpy(rows).cuda()
     g_qkv = host(qkv[idx])
     g_y = host(y[idx])
