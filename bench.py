@@ -303,23 +303,22 @@ def run_cost_table(args):
                 vl = B.Varlen([0, T], [0, L], [c.grid])
                 ws = torch.empty(B.block_workspace_size(cfg, vl), dtype=torch.uint8, device="cuda")
                 mod = torch.empty((1, 6, D), dtype=torch.float32, device="cuda")
-                qkv = torch.empty((T, 3 * D), dtype=torch.bfloat16, device="cuda")
+                qkv = torch.empty((3, T, D), dtype=torch.bfloat16, device="cuda")   # q, k, v planes
                 o = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
                 y = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
                 xs = x[:T]
                 if deg > 1:
                     Ha, n = H // deg, c.tokens
-                    qkv_a = normal((n, 3, Ha * hd))
+                    qkv_a = normal((3, n, Ha * hd))
                     o_a = torch.empty((n, Ha * hd), dtype=torch.bfloat16, device="cuda")
                     o_rows = normal((T, D))
 
                 def share():
                     B.block_pre_attention(cfg, w, vl, xs, t, mod, qkv, ws)
                     if deg > 1:
-                        B.attention_varlen(qkv_a[:, 0], qkv_a[:, 1], qkv_a[:, 2], o_a, [0, c.tokens], [0, c.tokens],
-                                           Ha, hd)
+                        B.attention_varlen(qkv_a[0], qkv_a[1], qkv_a[2], o_a, [0, c.tokens], [0, c.tokens], Ha, hd)
                     else:
-                        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, [0, T], [0, T], H, hd)
+                        B.attention_varlen(qkv[0], qkv[1], qkv[2], o, [0, T], [0, T], H, hd)
                     B.block_post_attention(cfg, w, vl, xs, o_rows if deg > 1 else o, txt, mod, y, ws)
 
                 for _ in range(args.warmup):
@@ -478,11 +477,11 @@ def profile_kernel(args, wl):
     T, D, H, hd = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
     g = torch.Generator(device="cuda")
     g.manual_seed(13501)
-    qkv = torch.randn((T, 3 * D), generator=g, device="cuda").to(torch.bfloat16)
+    qkv = torch.randn((3, T, D), generator=g, device="cuda").to(torch.bfloat16)   # q, k, v planes
     o = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
     cu = wl.cu_seqlens()
     for _ in range(args.steps):
-        B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
+        B.attention_varlen(qkv[0], qkv[1], qkv[2], o, cu, cu, H, hd)
     torch.cuda.synchronize()
     print(json.dumps({"profile": "attention", "workload": wl.name, "launches": args.steps}), flush=True)
 
@@ -666,7 +665,7 @@ def main():
     T, D, H, hd = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
     y = torch.empty_like(d["x"])
     mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
-    qkv = torch.empty((T, 3 * D), dtype=tdt, device="cuda")
+    qkv = torch.empty((3, T, D), dtype=tdt, device="cuda")   # q, k, v planes, as pre-attention writes them
     o = torch.empty((T, D), dtype=tdt, device="cuda")
     cu = wl.cu_seqlens()
     stream = torch.cuda.current_stream()
@@ -679,7 +678,7 @@ def main():
         g = torch.Generator(device="cuda")
         g.manual_seed(13501)
         Ha, cu_a = wl.attn_heads, wl.cu_attn()
-        qkv_a = torch.randn((cu_a[-1], 3, Ha * hd), generator=g, device="cuda").to(tdt)
+        qkv_a = torch.randn((3, cu_a[-1], Ha * hd), generator=g, device="cuda").to(tdt)
         o_a = torch.empty((cu_a[-1], Ha * hd), dtype=tdt, device="cuda")
         o_rows = torch.randn((T, D), generator=g, device="cuda").to(tdt)
 
@@ -688,9 +687,9 @@ def main():
         if ev is not None:
             ev[0].record(stream)
         if sp:
-            B.attention_varlen(qkv_a[:, 0], qkv_a[:, 1], qkv_a[:, 2], o_a, cu_a, cu_a, Ha, hd)
+            B.attention_varlen(qkv_a[0], qkv_a[1], qkv_a[2], o_a, cu_a, cu_a, Ha, hd)
         else:
-            B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, H, hd)
+            B.attention_varlen(qkv[0], qkv[1], qkv[2], o, cu, cu, H, hd)
         if ev is not None:
             ev[1].record(stream)
         B.block_post_attention(cfg, w, vl, d["x"], o_rows if sp else o, d["txt"], mod, y, ws)

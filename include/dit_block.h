@@ -47,7 +47,7 @@ extern "C" {
 #endif
 
 #define DIT_MAX_REQ 64
-#define DIT_ABI_VERSION 3
+#define DIT_ABI_VERSION 4
 
 typedef enum {
   DIT_OK = 0,
@@ -137,8 +137,10 @@ dit_status dit_block_forward(const dit_block_config *cfg, const dit_block_weight
  * projection, per-head RMSNorm and rotary on q and k.  With t != NULL (device
  * fp32 [n_req]) the modulation mod = adaLN(t) is computed and written to mod
  * (device fp32 [n_req, 6, D]); with t == NULL, mod is read as given.
- * qkv: [rows, 3D] with q in columns [0,D), k in [D,2D), v in [2D,3D), head j
- * at j*d within each (written). */
+ * qkv: three planes [3, rows, D] (written): q = qkv[0], k = qkv[1],
+ * v = qkv[2], each row-major with row stride D, head j in columns
+ * [j*d, (j+1)*d).  Separate planes keep each row kernel's and attention's
+ * reads on whole contiguous rows. */
 dit_status dit_block_pre_attention(const dit_block_config *cfg, const dit_block_weights *w,
                                    const dit_varlen *vl, const void *x, const float *t,
                                    float *mod, void *qkv, void *ws, size_t ws_bytes,

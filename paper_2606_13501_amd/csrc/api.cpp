@@ -252,11 +252,12 @@ dit_status check_ws(const dit_block_config* c, const dit_varlen* vl, void* ws, s
 dit_status run_linear(const void* a, int64_t lda, const void* w, int64_t ldw, const void* bias, void* out,
                       int64_t ldo, int64_t M, int N, int K, dit_epilogue epi, const void* res, int64_t ldr,
                       const float* gate, int64_t gate_stride, const ReqTable& req, dit_dtype dt,
-                      hipStream_t s, const char* what) {
+                      hipStream_t s, const char* what, int plane_cols = 0, int64_t plane_stride = 0) {
   LinearArgs p;
   p.a = a; p.lda = lda; p.w = w; p.ldw = ldw; p.bias = bias; p.out = out; p.ldo = ldo;
   p.M = M; p.N = N; p.K = K; p.epi = epi; p.res = res; p.ldr = ldr; p.gate = gate;
   p.gate_stride = gate_stride; p.req = req; p.dtype = dt;
+  p.plane_cols = plane_cols; p.plane_stride = plane_stride;
   return hip_status(launch_linear(p, s), what);
 }
 
@@ -312,7 +313,9 @@ dit_status run_cond(const dit_block_config* c, const dit_block_weights* w, int n
   return hip_status(launch_conditioning(p, s), "timestep conditioning");
 }
 
-// S1..S3 on this GPU's rows: h = LN(x)(1+scale_sa)+shift_sa; qkv = h W^T + b; q,k RMSNorm + rotary.
+// S1..S3 on this GPU's rows: h = LN(x)(1+scale_sa)+shift_sa; [q|k|v] = h W^T + b; q,k RMSNorm + rotary.
+// q, k and v are written as three planes [T, D] (row stride D), T * D elements apart: the row
+// kernels and attention then read contiguous rows of one tensor.
 dit_status pre_attention_impl(const dit_block_config* c, const dit_block_weights* w, const dit_varlen* vl,
                               const void* x, const float* mod, void* qkv, const Workspace& ws,
                               hipStream_t s) {
@@ -322,13 +325,24 @@ dit_status pre_attention_impl(const dit_block_config* c, const dit_block_weights
   RopeTable tab;
   DIT_TRY(check_rope_table(vl, c->rope_sections, &tab));
   DIT_TRY(run_ln_mod(x, mod + 0 * D, mod + 1 * D, 6 * D, req, T, D, c->ln_eps, ws.h, c->dtype, s));
-  DIT_TRY(run_linear(ws.h, D, w->w_qkv, D, w->b_qkv, qkv, 3 * D, T, 3 * D, D, DIT_EPI_NONE, nullptr, 0, nullptr,
-                     0, req, c->dtype, s, "qkv projection"));
+  DIT_TRY(run_linear(ws.h, D, w->w_qkv, D, w->b_qkv, qkv, D, T, 3 * D, D, DIT_EPI_NONE, nullptr, 0, nullptr,
+                     0, req, c->dtype, s, "qkv projection", D, T * D));
   const size_t es = elem_size(c->dtype);
-  DIT_TRY(run_norm_rope(qkv, (char*)qkv + D * es, 3 * D, T, c->n_heads, c->head_dim, c->qk_norm ? w->g_q : nullptr,
+  DIT_TRY(run_norm_rope(qkv, (char*)qkv + T * D * es, D, T, c->n_heads, c->head_dim, c->qk_norm ? w->g_q : nullptr,
                         c->qk_norm ? w->g_k : nullptr, c->rms_eps, c->rope_sections, c->rope_theta, &tab,
                         c->dtype, s));
   return DIT_OK;
+}
+
+// Self-attention of one block over the q, k, v planes that pre_attention_impl wrote.
+dit_status self_attention_impl(const dit_block_config* c, const dit_varlen* vl, const char* qkv, void* o,
+                               hipStream_t s) {
+  const int D = c->hidden;
+  const int64_t T = vl->cu_seqlens[vl->n_req];
+  const size_t plane = (size_t)T * D * elem_size(c->dtype);
+  const ReqTable req = make_req(vl->cu_seqlens, vl->n_req);
+  return run_attention(qkv, qkv + plane, qkv + 2 * plane, o, D, D, D, D, req, req, c->n_heads, c->head_dim,
+                       1.0f / sqrtf((float)c->head_dim), c->dtype, s);
 }
 
 // Cross-attention keys and values of one block: kv = [RMS(txt W_ck^T + b_ck) | txt W_cv^T + b_cv].
@@ -631,17 +645,13 @@ dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weight
   DIT_TRY(check_ptr(y, "y"));
   Workspace W;
   DIT_TRY(check_ws(cfg, vl, ws, ws_bytes, &W));
-  const int D = cfg->hidden;
-  const size_t es = elem_size(cfg->dtype);
-  const ReqTable req = make_req(vl->cu_seqlens, vl->n_req);
   const float* m = mod;
   if (!m) {
     DIT_TRY(run_cond(cfg, w, vl->n_req, t, W.mod, W.e, W.a1, W.c, stream));
     m = W.mod;
   }
   DIT_TRY(pre_attention_impl(cfg, w, vl, x, m, W.qkv, W, stream));
-  DIT_TRY(run_attention(W.qkv, W.qkv + D * es, W.qkv + 2 * D * es, W.o, 3 * D, 3 * D, 3 * D, D, req, req,
-                        cfg->n_heads, cfg->head_dim, 1.0f / sqrtf((float)cfg->head_dim), cfg->dtype, stream));
+  DIT_TRY(self_attention_impl(cfg, vl, W.qkv, W.o, stream));
   return post_attention_impl(cfg, w, vl, x, W.o, txt, m, y, W, stream);
 }
 
@@ -914,7 +924,6 @@ dit_status dit_denoise_step(const dit_model_config* cfg, const dit_model_weights
   const size_t es = elem_size(c->dtype);
   const dit_dtype dty = c->dtype;
   const ReqTable req = make_req(vl->cu_seqlens, R);
-  const float scale = 1.0f / sqrtf((float)c->head_dim);
   // x = patchify(latent) W_pe^T + b_pe
   DIT_TRY(run_latent(false, cfg, tab, latent, W.tok, nullptr, nullptr, stream));
   DIT_TRY(run_linear(W.tok, P, w->w_pe, P, w->b_pe, W.x, D, T, D, P, DIT_EPI_NONE, nullptr, 0, nullptr, 0, req, dty,
@@ -928,8 +937,7 @@ dit_status dit_denoise_step(const dit_model_config* cfg, const dit_model_weights
     DIT_TRY(run_cond_parts(c, R, t, nullptr, nullptr, nullptr, nullptr, bw->w_ada, bw->b_ada, 6, B.mod, B, stream,
                            "block modulation"));
     DIT_TRY(pre_attention_impl(c, bw, vl, W.x, B.mod, B.qkv, B, stream));
-    DIT_TRY(run_attention(B.qkv, B.qkv + D * es, B.qkv + 2 * D * es, B.o, 3 * D, 3 * D, 3 * D, D, req, req,
-                          c->n_heads, c->head_dim, scale, dty, stream));
+    DIT_TRY(self_attention_impl(c, vl, B.qkv, B.o, stream));
     DIT_TRY(post_attention_impl(c, bw, vl, W.x, B.o, nullptr, B.mod, W.x, B, stream,
                                 (const char*)kv + (size_t)b * L * 2 * D * es));
   }

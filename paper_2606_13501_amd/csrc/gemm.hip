@@ -123,7 +123,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     const bf16* __restrict__ A, int64_t lda, const bf16* __restrict__ W, int64_t ldw,
     const bf16* __restrict__ bias, bf16* __restrict__ C, int64_t ldc, const bf16* R, int64_t ldr,
     const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K,
-    int tiles_m, int tiles_n) {
+    int tiles_m, int tiles_n, int plane_cols, int64_t plane_skip) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes + kWaves * kEpiBytes];
 
   const TileSeq seq = tile_seq(blockIdx.x, gridDim.x, tiles_m, tiles_n);
@@ -374,9 +374,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   char* const ew = smem + kStages * kStageBytes + wave * kEpiBytes;
   const int er = lane >> 4, ec = lane & 15;   // read role: rows er + 4 k, chunk ec
   float bsum[2][4];
+  int64_t c_off[2];   // output plane of the lane's 4 columns (planes: column n in plane n / plane_cols)
 #pragma unroll
   for (int ih = 0; ih < 2; ++ih) {
     const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+    c_off[ih] = plane_cols > 0 ? (int64_t)(n / plane_cols) * plane_skip : 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) bsum[ih][e] = 0.f;
     if (bias && n < N) {
@@ -459,7 +461,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
           bf16x4 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) o[e] = (bf16)z[e];
-          *reinterpret_cast<bf16x4*>(C + (int64_t)m * ldc + n) = o;
+          *reinterpret_cast<bf16x4*>(C + c_off[ih] + (int64_t)m * ldc + n) = o;
         }
       }
     }
@@ -485,7 +487,8 @@ template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_nt(
     const float* __restrict__ A, int64_t lda, const float* __restrict__ W, int64_t ldw,
     const float* __restrict__ bias, float* C, int64_t ldc, const float* R, int64_t ldr,
-    const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K) {
+    const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K, int plane_cols,
+    int64_t plane_skip) {
   __shared__ float As[FK][FT + 1];
   __shared__ float Ws[FK][FT + 1];
   const int m0 = blockIdx.y * FT, n0 = blockIdx.x * FT;
@@ -528,7 +531,7 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(
       if (EPI == DIT_EPI_GELU_TANH) z = gelu_tanh(z);
       else if (EPI == DIT_EPI_RESIDUAL) z = R[(int64_t)m * ldr + n] + z;
       else if (EPI == DIT_EPI_GATED_RESIDUAL) z = R[(int64_t)m * ldr + n] + g[n] * z;
-      C[(int64_t)m * ldc + n] = z;
+      C[(plane_cols > 0 ? (int64_t)(n / plane_cols) * plane_skip : 0) + (int64_t)m * ldc + n] = z;
     }
   }
 }
@@ -559,11 +562,15 @@ hipError_t launch_bf16(const LinearArgs& p, hipStream_t s) {
     if (resident >= kXcds && grid > resident) grid = resident;
     gemm_bf16_nt<EPI, true><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
-        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n);
+        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
+        p.plane_cols,
+        p.plane_stride - p.plane_cols);
   } else {
     gemm_bf16_nt<EPI, false><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
-        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n);
+        (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
+        p.plane_cols,
+        p.plane_stride - p.plane_cols);
   }
   return hipGetLastError();
 }
@@ -573,7 +580,8 @@ hipError_t launch_f32(const LinearArgs& p, hipStream_t s) {
   dim3 grid((p.N + FT - 1) / FT, (unsigned)((p.M + FT - 1) / FT));
   gemm_f32_nt<EPI><<<grid, 256, 0, s>>>(
       (const float*)p.a, p.lda, (const float*)p.w, p.ldw, (const float*)p.bias, (float*)p.out, p.ldo,
-      (const float*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K);
+      (const float*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, p.plane_cols,
+      p.plane_stride - p.plane_cols);
   return hipGetLastError();
 }
 

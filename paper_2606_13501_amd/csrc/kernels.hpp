@@ -21,6 +21,11 @@ struct LinearArgs {
   const float* gate; int64_t gate_stride;
   ReqTable req;
   dit_dtype dtype;
+  // plane_cols > 0: output column n goes to plane n / plane_cols, column
+  // n % plane_cols, planes plane_stride elements apart (ldo = plane_cols);
+  // plane_cols a multiple of 4
+  int plane_cols = 0;
+  int64_t plane_stride = 0;
 };
 hipError_t launch_linear(const LinearArgs& p, hipStream_t s);
 

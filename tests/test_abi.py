@@ -43,7 +43,7 @@ def test_library_exports_every_header_function():
 
 def test_abi_version_and_strings():
     L = _lib()
-    assert L.dit_abi_version() == 3
+    assert L.dit_abi_version() == 4
     assert L.dit_status_string(B.DIT_ERR_WORKSPACE) == b"workspace too small"
     assert L.dit_status_string(B.DIT_OK) == b"ok"
 

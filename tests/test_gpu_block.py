@@ -55,11 +55,11 @@ def test_block_seams_compose_to_forward():
     y_ref = db.forward()
     T, D = wl.n_rows, wl.hidden
     mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
-    qkv = empty((T, 3 * D), "bf16")
+    qkv = empty((3, T, D), "bf16")
     B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, qkv, db.ws)
     o = empty((T, D), "bf16")
     cu = wl.cu_seqlens()
-    B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, wl.n_heads, wl.head_dim)
+    B.attention_varlen(qkv[0], qkv[1], qkv[2], o, cu, cu, wl.n_heads, wl.head_dim)
     y = empty((T, D), "bf16")
     B.block_post_attention(db.cfg, db.w, db.vl, db.d["x"], o, db.d["txt"], mod, y, db.ws)
     torch.cuda.synchronize()
@@ -120,16 +120,16 @@ def test_shard_rows_equal_full_rows():
     B = db.B
     D = wl.hidden
     mod = torch.empty((1, 6, D), dtype=torch.float32, device="cuda")
-    full = empty((513, 3 * D), "bf16")
+    full = empty((3, 513, D), "bf16")
     B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, full, db.ws)
     a, b = 171, 342
     vls = B.Varlen([0, b - a], [0, 64], [(3, 9, 19)], [a])
-    shard = empty((b - a, 3 * D), "bf16")
+    shard = empty((3, b - a, D), "bf16")
     xs = db.d["x"][a:b].contiguous()
     ws = torch.empty(B.block_workspace_size(db.cfg, vls), dtype=torch.uint8, device="cuda")
     B.block_pre_attention(db.cfg, db.w, vls, xs, db.d["t"], mod, shard, ws)
     torch.cuda.synchronize()
-    assert torch.equal(shard, full[a:b])
+    assert torch.equal(shard, full[:, a:b])
 
 
 def test_block_forward_with_precomputed_modulation():
@@ -170,11 +170,11 @@ def test_block_seams_with_precomputed_modulation():
     y_ref = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
     B.block_forward(db.cfg, w2, db.vl, db.d["x"], None, db.d["txt"], y_ref, db.ws, mod=mod)
     mod_in = mod.clone()
-    qkv = empty((T, 3 * D), "bf16")
+    qkv = empty((3, T, D), "bf16")
     B.block_pre_attention(db.cfg, w2, db.vl, db.d["x"], None, mod_in, qkv, db.ws)
     o = empty((T, D), "bf16")
     cu = wl.cu_seqlens()
-    B.attention_varlen(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], o, cu, cu, wl.n_heads, wl.head_dim)
+    B.attention_varlen(qkv[0], qkv[1], qkv[2], o, cu, cu, wl.n_heads, wl.head_dim)
     y = empty((T, D), "bf16")
     B.block_post_attention(db.cfg, w2, db.vl, db.d["x"], o, db.d["txt"], mod_in, y, db.ws)
     y_t = empty((T, D), "bf16")

@@ -35,20 +35,17 @@ def test_self_attention_full_size(name):
     log(f"case full-size self-attention {name}: rows {wl.cu_attn()[-1]} heads {H}")
     att = synth.generate_attention_inputs(wl)
     T = att["q"].shape[0]
-    qkv = np.empty((T, 3 * W), dtype=np.uint16)   # packed like the block's qkv buffer
-    qkv[:, :W] = att["q"].reshape(T, W)
-    qkv[:, W:2 * W] = att["k"].reshape(T, W)
-    qkv[:, 2 * W:] = att["v"].reshape(T, W)
+    # three planes [3, T, W], as the block's pre-attention steps write them
+    qkv = np.stack([att[n].reshape(T, W) for n in ("q", "k", "v")])
     t = dev(qkv)
     o = empty((T, W), "bf16")
     cu = wl.cu_attn()
-    B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], o, cu, cu, H, d)
+    B.attention_varlen(t[0], t[1], t[2], o, cu, cu, H, d)
     torch.cuda.synchronize()
     rows = synth.generate_sampled_rows(wl, 2048, sample_id=3, attn=True)
     g = host(o[torch.from_numpy(rows).cuda()])
     del t, o
-    ref = O.attention_varlen(O.decode(qkv[:, :W]), O.decode(qkv[:, W:2 * W]), O.decode(qkv[:, 2 * W:]), cu, cu, H, d,
-                             q_rows=rows)
+    ref = O.attention_varlen(O.decode(qkv[0]), O.decode(qkv[1]), O.decode(qkv[2]), cu, cu, H, d, q_rows=rows)
     check(g, ref, "bf16", f"{name} self-attention ({len(rows)} sampled rows)")
 
 
@@ -60,7 +57,7 @@ def test_pre_post_attention_full_size(name):
     B = db.B
     T, D = wl.n_rows, wl.hidden
     mod = torch.empty((wl.n_req, 6, D), dtype=torch.float32, device="cuda")
-    qkv = empty((T, 3 * D), "bf16")
+    qkv = empty((3, T, D), "bf16")
     B.block_pre_attention(db.cfg, db.w, db.vl, db.d["x"], db.d["t"], mod, qkv, db.ws)
     o_in = synth.generate_attention_inputs(wl)["o"]
     y = empty((T, D), "bf16")
@@ -69,7 +66,7 @@ def test_pre_post_attention_full_size(name):
     rows = synth.generate_sampled_rows(wl, 2048, sample_id=4, tile=256)
     log(f"  {len(rows)} sampled rows (every 256-row tile's first and last row among them)")
     idx = torch.from_numpy(rows).cuda()
-    g_qkv = host(qkv[idx])
+    g_qkv = host(qkv[:, idx])
     g_y = host(y[idx])
     g_mod = host(mod)
     del qkv, y
@@ -77,9 +74,9 @@ def test_pre_post_attention_full_size(name):
     ref_mod = O.conditioning(w["t"], wl.freq_dim, w)
     check(g_mod, ref_mod, "bf16", f"{name} modulation")
     q, k, v = oracle_pre_rows(wl, w, ref_mod, rows)
-    check(g_qkv[:, :D], q, "bf16", f"{name} q")
-    check(g_qkv[:, D:2 * D], k, "bf16", f"{name} k")
-    check(g_qkv[:, 2 * D:], v, "bf16", f"{name} v")
+    check(g_qkv[0], q, "bf16", f"{name} q")
+    check(g_qkv[1], k, "bf16", f"{name} k")
+    check(g_qkv[2], v, "bf16", f"{name} v")
     ref_y = oracle_post_rows(wl, w, ref_mod, O.decode(o_in), rows)
     x = w["x"][rows]
     check(g_y, ref_y, "bf16", f"{name} post-attention y")
