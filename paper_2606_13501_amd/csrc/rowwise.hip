@@ -28,11 +28,38 @@ template <> struct Vec16<float> { typedef f32x4 type; static constexpr int n = 4
 //   affine:   mul = gamma, add = beta (dtype vectors)
 // NVL = 16-byte vectors per lane, a compile-time count so the row is held in
 // exactly as many registers as it needs (occupancy hides the HBM latency).
-template <typename T, bool AFFINE, int NVL>
-__global__ __launch_bounds__(256) void layer_norm_kernel(
+
+// Mean and 1 / sqrt(var + eps) of the wave's row v (NVL vectors per lane).
+// The squares are accumulated with explicit fused multiply-adds, so every
+// kernel that calls this rounds the statistics the same way.
+template <typename T, int NVL, typename V>
+__device__ __forceinline__ void row_stats(const V (&v)[NVL], int lane, int nv, int hidden, float eps, float& mean,
+                                          float& rstd) {
+  constexpr int VN = Vec16<T>::n;
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NVL; ++i)
+#pragma unroll
+    for (int e = 0; e < VN; ++e) sum += to_f<T>(v[i][e]);
+  mean = wave_sum(sum) / hidden;
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < NVL; ++i) {
+    if (lane + 64 * i < nv) {
+#pragma unroll
+      for (int e = 0; e < VN; ++e) {
+        const float d = to_f<T>(v[i][e]) - mean;
+        sq = fmaf(d, d, sq);
+      }
+    }
+  }
+  rstd = rsqrtf(wave_sum(sq) / hidden + eps);
+}
+
+template <typename T, int NVL>
+__global__ __launch_bounds__(256) void layer_norm_affine_kernel(
     const T* __restrict__ x, T* __restrict__ out, int64_t n_rows, int hidden, float eps,
-    const float* __restrict__ shift, const float* __restrict__ scale, int64_t mod_stride,
-    const T* __restrict__ gamma, const T* __restrict__ beta, ReqTable req) {
+    const T* __restrict__ gamma, const T* __restrict__ beta) {
   typedef typename Vec16<T>::type V;
   constexpr int VN = Vec16<T>::n;
   const int lane = threadIdx.x & 63;
@@ -41,61 +68,107 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(
   const int nv = hidden / VN;
   const T* xr = x + row * hidden;
   V v[NVL];
-  float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < NVL; ++i) {
     const int c = lane + 64 * i;
     v[i] = c < nv ? __builtin_nontemporal_load(reinterpret_cast<const V*>(xr + c * VN)) : V{};
   }
-#pragma unroll
-  for (int i = 0; i < NVL; ++i)
-#pragma unroll
-    for (int e = 0; e < VN; ++e) sum += to_f<T>(v[i][e]);
-  const float mean = wave_sum(sum) / hidden;
-  float sq = 0.f;
-#pragma unroll
-  for (int i = 0; i < NVL; ++i) {
-    const int c = lane + 64 * i;
-    if (c < nv) {
-#pragma unroll
-      for (int e = 0; e < VN; ++e) {
-        float d = to_f<T>(v[i][e]) - mean;
-        sq += d * d;
-      }
-    }
-  }
-  const float rstd = rsqrtf(wave_sum(sq) / hidden + eps);
-  const float* sh = nullptr;
-  const float* sc = nullptr;
-  if (!AFFINE) {
-    const int r = find_req(req.cu, req.n_req, (int)row);
-    sh = shift + (int64_t)r * mod_stride;
-    sc = scale + (int64_t)r * mod_stride;
-  }
+  float mean, rstd;
+  row_stats<T, NVL>(v, lane, nv, hidden, eps, mean, rstd);
   T* orow = out + row * hidden;
 #pragma unroll
   for (int i = 0; i < NVL; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
+      const V g = *reinterpret_cast<const V*>(gamma + c * VN);
+      const V b = *reinterpret_cast<const V*>(beta + c * VN);
       V o;
-      if (AFFINE) {
-        V g = *reinterpret_cast<const V*>(gamma + c * VN);
-        V b = *reinterpret_cast<const V*>(beta + c * VN);
 #pragma unroll
-        for (int e = 0; e < VN; ++e)
-          o[e] = from_f<T>((to_f<T>(v[i][e]) - mean) * rstd * to_f<T>(g[e]) + to_f<T>(b[e]));
-      } else {
-#pragma unroll
-        for (int e = 0; e < VN; e += 4) {
-          f32x4 s4 = *reinterpret_cast<const f32x4*>(sc + c * VN + e);
-          f32x4 h4 = *reinterpret_cast<const f32x4*>(sh + c * VN + e);
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            o[e + u] = from_f<T>((to_f<T>(v[i][e + u]) - mean) * rstd * (1.0f + s4[u]) + h4[u]);
-        }
-      }
+      for (int e = 0; e < VN; ++e)
+        o[e] = from_f<T>(fmaf((to_f<T>(v[i][e]) - mean) * rstd, to_f<T>(g[e]), to_f<T>(b[e])));
       __builtin_nontemporal_store(o, reinterpret_cast<V*>(orow + c * VN));
     }
+  }
+}
+
+// Modulated LayerNorm, WAVES rows per workgroup.  When all of them belong to
+// one request (every workgroup but those across a request boundary), the
+// request's 1 + scale and shift are first staged in LDS as fp32 (8 bytes per
+// column), so they are read from L2 once per workgroup rather than once per
+// row: at 75,600 x 5,120 the per-row reads were 40 KB of L2 traffic for
+// every 10 KB row, and staging took the kernel from 70% to 75% of the HBM
+// peak.  The other workgroups read the vectors of each row's request
+// directly; both paths round identically.  The row is loaded after the
+// staging: issued before it, the row loads held the staged reads back
+// behind them and the kernel ran 20% slower.
+template <typename T, int NVL, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void layer_norm_mod_kernel(
+    const T* __restrict__ x, T* __restrict__ out, int64_t n_rows, int hidden, float eps,
+    const float* __restrict__ shift, const float* __restrict__ scale, int64_t mod_stride, ReqTable req) {
+  typedef typename Vec16<T>::type V;
+  constexpr int VN = Vec16<T>::n;
+  extern __shared__ f32x4 smod[];   // hidden / 4 vectors of 1 + scale, then hidden / 4 of shift
+  const int lane = threadIdx.x & 63;
+  const int64_t r0 = (int64_t)blockIdx.x * WAVES;
+  const int64_t row = r0 + (threadIdx.x >> 6);
+  const int ra = find_req(req.cu, req.n_req, (int)r0);
+  const bool staged = ra == find_req(req.cu, req.n_req, (int)(min(r0 + WAVES, n_rows) - 1));
+  const int nv = hidden / VN, h4 = hidden / 4;
+  if (staged) {   // uniform over the workgroup
+    const f32x4* sc = reinterpret_cast<const f32x4*>(scale + (int64_t)ra * mod_stride);
+    const f32x4* sh = reinterpret_cast<const f32x4*>(shift + (int64_t)ra * mod_stride);
+    for (int i = threadIdx.x; i < h4; i += WAVES * 64) {
+      f32x4 m = sc[i];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) m[u] = 1.0f + m[u];
+      smod[i] = m;
+      smod[h4 + i] = sh[i];
+    }
+    __syncthreads();
+  }
+  if (row >= n_rows) return;
+  V v[NVL];
+  {
+    const T* xr = x + row * hidden;
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int c = lane + 64 * i;
+      v[i] = c < nv ? __builtin_nontemporal_load(reinterpret_cast<const V*>(xr + c * VN)) : V{};
+    }
+  }
+  float mean, rstd;
+  row_stats<T, NVL>(v, lane, nv, hidden, eps, mean, rstd);
+  const int r = staged ? ra : find_req(req.cu, req.n_req, (int)row);
+  const f32x4* sc = reinterpret_cast<const f32x4*>(scale + (int64_t)r * mod_stride);
+  const f32x4* sh = reinterpret_cast<const f32x4*>(shift + (int64_t)r * mod_stride);
+  T* orow = out + row * hidden;
+  auto emit = [&](auto&& mul_add) {
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        V o;
+#pragma unroll
+        for (int e = 0; e < VN; e += 4) {
+          f32x4 m4, a4;
+          mul_add((c * VN + e) / 4, m4, a4);
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            o[e + u] = from_f<T>(fmaf((to_f<T>(v[i][e + u]) - mean) * rstd, m4[u], a4[u]));
+        }
+        __builtin_nontemporal_store(o, reinterpret_cast<V*>(orow + c * VN));
+      }
+    }
+  };
+  if (staged) {
+    emit([&](int j, f32x4& m4, f32x4& a4) { m4 = smod[j]; a4 = smod[h4 + j]; });
+  } else {
+    emit([&](int j, f32x4& m4, f32x4& a4) {
+      m4 = sc[j];
+      a4 = sh[j];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) m4[u] = 1.0f + m4[u];
+    });
   }
 }
 
@@ -322,17 +395,18 @@ hipError_t gres_typed(const GatedResArgs& p, hipStream_t s) {
   }
 }
 
+constexpr int kLnModWaves = 4;   // rows of the modulated LayerNorm per workgroup
+
 template <typename T, int NVL>
 hipError_t ln_nvl(const LnArgs& p, hipStream_t s) {
-  const unsigned grid = (unsigned)((p.n_rows + 3) / 4);
-  if (p.affine)
-    layer_norm_kernel<T, true, NVL><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
-                                                         nullptr, nullptr, 0, (const T*)p.gamma,
-                                                         (const T*)p.beta, p.req);
-  else
-    layer_norm_kernel<T, false, NVL><<<grid, 256, 0, s>>>((const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps,
-                                                          p.shift, p.scale, p.mod_stride, nullptr, nullptr,
-                                                          p.req);
+  if (p.affine) {
+    layer_norm_affine_kernel<T, NVL><<<(unsigned)((p.n_rows + 3) / 4), 256, 0, s>>>(
+        (const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps, (const T*)p.gamma, (const T*)p.beta);
+  } else {
+    layer_norm_mod_kernel<T, NVL, kLnModWaves>
+        <<<(unsigned)((p.n_rows + kLnModWaves - 1) / kLnModWaves), kLnModWaves * 64, (size_t)p.hidden * 8, s>>>(
+            (const T*)p.x, (T*)p.out, p.n_rows, p.hidden, p.eps, p.shift, p.scale, p.mod_stride, p.req);
+  }
   return hipGetLastError();
 }
 
