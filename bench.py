@@ -486,35 +486,6 @@ def profile_kernel(args, wl):
     print(json.dumps({"profile": "attention", "workload": wl.name, "launches": args.steps}), flush=True)
 
 
-def gpu_clocks():
-    """Current graphics clock, memory clock and power of GPU 0 from amd-smi, or
-    None where the tool is not available."""
-    import subprocess
-    try:
-        r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--power", "--json"], capture_output=True,
-                           text=True, timeout=30)
-        data = json.loads(r.stdout)
-    except Exception:
-        return None
-    out = {}
-
-    def walk(x, path):
-        if isinstance(x, dict):
-            if "value" in x and not isinstance(x["value"], (dict, list)):
-                out[path] = f"{x['value']} {x.get('unit', '')}".strip()
-                return
-            for k, v in x.items():
-                walk(v, f"{path}.{k}" if path else k)
-        elif isinstance(x, list):
-            for i, v in enumerate(x):
-                walk(v, path)
-
-    walk(data, "")
-    keep = {k: v for k, v in out.items()
-            if any(t in k for t in ("gfx_0.clk", "mem_0.clk", "socket_power", "current_socket_power"))}
-    return keep or None
-
-
 def oracle_seconds(wl):
     """The float64 oracle on the workload's whole block, as it stands, on the
     host cores, timed by stages: conditioning and pre-attention on the rows,
@@ -697,7 +668,6 @@ def main():
     def new_ev():
         return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
-    clocks_before = gpu_clocks()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -715,7 +685,6 @@ def main():
     ms = start.elapsed_time(stop) / args.steps
     attn_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
     step_ms = sorted(a.elapsed_time(b) for a, b in sevs)
-    clocks_after = gpu_clocks()
 
     # cold: a 1 GiB scratch write between steps evicts the inputs from the caches
     cold = None
@@ -771,7 +740,6 @@ def main():
             "ms_step_median": round(step_ms[len(step_ms) // 2], 3), "ms_step_min": round(step_ms[0], 3),
             "ms_step_cold_median": round(cold[len(cold) // 2], 3) if cold else None,
             "ms_step_cold_min": round(cold[0], 3) if cold else None,
-            "gpu_clocks_before": clocks_before, "gpu_clocks_after": clocks_after,
         },
         "roofline": {
             "kernel": "attn_fwd_bf16 (self-attention)" if wl.dtype == "bf16" else "attn_fwd_f32 (self-attention)",

@@ -359,6 +359,46 @@ dit_status text_kv_impl(const dit_block_config* c, const dit_block_weights* w, i
   return DIT_OK;
 }
 
+// A second stream per device (default priority) with a fork and a join
+// event, for the text key/value projection: it depends on the text and the
+// weights only, so it runs beside the output projection, LayerNorm and
+// cross-query projection instead of after them.  Where those leave compute
+// units idle (a short sequence: 192 tiles of 256 x 256 on 256 CUs) its tiles
+// fill them.  The mutex covers a call's enqueue from fork to join, so calls
+// from several host threads never interleave their use of the two events.
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  std::mutex mu;
+};
+constexpr int kMaxSideDevices = 64;
+std::mutex g_side_mu;
+SideStream* g_side[kMaxSideDevices] = {};
+
+// The current device's side stream, created on first use; NULL if it cannot
+// be created (the caller then runs everything on its own stream).
+SideStream* side_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxSideDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  if (!g_side[dev]) {
+    SideStream* ss = new SideStream;
+    const bool ok = hipStreamCreateWithFlags(&ss->stream, hipStreamNonBlocking) == hipSuccess &&
+                    hipEventCreateWithFlags(&ss->fork, hipEventDisableTiming) == hipSuccess &&
+                    hipEventCreateWithFlags(&ss->join, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+      if (ss->join) (void)hipEventDestroy(ss->join);
+      if (ss->fork) (void)hipEventDestroy(ss->fork);
+      if (ss->stream) (void)hipStreamDestroy(ss->stream);
+      delete ss;
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_side[dev] = ss;
+  }
+  return g_side[dev];
+}
+
 // S5..S12 on this GPU's rows given the self-attention output o.
 // With kv != NULL the text keys and values come from that cache ([txt_rows, 2D],
 // normalised keys) and txt is not read.
@@ -372,6 +412,23 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   const ReqTable req = make_req(vl->cu_seqlens, vl->n_req);
   const ReqTable req_txt = make_req(vl->cu_seqlens_txt, vl->n_req);
   const dit_dtype dt = c->dtype;
+  // [ck | cv] = txt W_ckv^T + b_ckv ; ck = RMS(ck), on the side stream when there is one
+  const char* ckv = (const char*)kv;
+  SideStream* side = nullptr;
+  std::unique_lock<std::mutex> side_lock;
+  if (!ckv) {
+    side = side_stream();
+    if (side) {
+      side_lock = std::unique_lock<std::mutex>(side->mu);
+      DIT_HIP(hipEventRecord(side->fork, s), "hipEventRecord");
+      DIT_HIP(hipStreamWaitEvent(side->stream, side->fork, 0), "hipStreamWaitEvent");
+      DIT_TRY(text_kv_impl(c, w, L, req_txt, txt, ws.ckv, side->stream));
+      DIT_HIP(hipEventRecord(side->join, side->stream), "hipEventRecord");
+    } else {
+      DIT_TRY(text_kv_impl(c, w, L, req_txt, txt, ws.ckv, s));
+    }
+    ckv = ws.ckv;
+  }
   // x1 = x + gate_sa (o W_o^T + b_o)
   DIT_TRY(run_linear(o, D, w->w_o, D, w->b_o, ws.x1, D, T, D, D, DIT_EPI_GATED_RESIDUAL, x, D, mod + 2 * D, 6 * D,
                      req, dt, s, "output projection"));
@@ -386,12 +443,7 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
     DIT_TRY(run_norm_rope(ws.cq, nullptr, D, T, c->n_heads, c->head_dim, w->g_cq, nullptr, c->rms_eps, zero, 0.f,
                           nullptr, dt, s));
   }
-  // [ck | cv] = txt W_ckv^T + b_ckv ; ck = RMS(ck)
-  const char* ckv = (const char*)kv;
-  if (!ckv) {
-    DIT_TRY(text_kv_impl(c, w, L, req_txt, txt, ws.ckv, s));
-    ckv = ws.ckv;
-  }
+  if (side) DIT_HIP(hipStreamWaitEvent(s, side->join, 0), "hipStreamWaitEvent");
   // oc = cross attention (queries: the request's latent rows, keys: its text rows)
   DIT_TRY(run_attention(ws.cq, ckv, ckv + D * es, ws.o, D, 2 * D, 2 * D, D, req, req_txt, c->n_heads,
                         c->head_dim, 1.0f / sqrtf((float)c->head_dim), dt, s,

@@ -107,7 +107,12 @@ __global__ __launch_bounds__(WAVES * 64) void layer_norm_mod_kernel(
     const float* __restrict__ shift, const float* __restrict__ scale, int64_t mod_stride, ReqTable req) {
   typedef typename Vec16<T>::type V;
   constexpr int VN = Vec16<T>::n;
-  extern __shared__ f32x4 smod[];   // hidden / 4 vectors of 1 + scale, then hidden / 4 of shift
+  // hidden / 4 vectors of 1 + scale, then hidden / 4 of shift.  Source vector
+  // j = G c + g (G = VN / 4 per 16-byte row vector c) is kept at g nv + c, so
+  // the 64 lanes of a read, and of a staging write, touch 64 consecutive
+  // vectors (no bank conflicts).
+  constexpr int G = VN / 4;
+  extern __shared__ f32x4 smod[];
   const int lane = threadIdx.x & 63;
   const int64_t r0 = (int64_t)blockIdx.x * WAVES;
   const int64_t row = r0 + (threadIdx.x >> 6);
@@ -117,12 +122,13 @@ __global__ __launch_bounds__(WAVES * 64) void layer_norm_mod_kernel(
   if (staged) {   // uniform over the workgroup
     const f32x4* sc = reinterpret_cast<const f32x4*>(scale + (int64_t)ra * mod_stride);
     const f32x4* sh = reinterpret_cast<const f32x4*>(shift + (int64_t)ra * mod_stride);
-    for (int i = threadIdx.x; i < h4; i += WAVES * 64) {
+    for (int at = threadIdx.x; at < h4; at += WAVES * 64) {   // consecutive LDS writes
+      const int i = G * (at % nv) + at / nv;
       f32x4 m = sc[i];
 #pragma unroll
       for (int u = 0; u < 4; ++u) m[u] = 1.0f + m[u];
-      smod[i] = m;
-      smod[h4 + i] = sh[i];
+      smod[at] = m;
+      smod[h4 + at] = sh[i];
     }
     __syncthreads();
   }
@@ -161,7 +167,11 @@ __global__ __launch_bounds__(WAVES * 64) void layer_norm_mod_kernel(
     }
   };
   if (staged) {
-    emit([&](int j, f32x4& m4, f32x4& a4) { m4 = smod[j]; a4 = smod[h4 + j]; });
+    emit([&](int j, f32x4& m4, f32x4& a4) {
+      const int at = (j % G) * nv + j / G;
+      m4 = smod[at];
+      a4 = smod[h4 + at];
+    });
   } else {
     emit([&](int j, f32x4& m4, f32x4& a4) {
       m4 = sc[j];
