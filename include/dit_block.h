@@ -228,6 +228,15 @@ dit_status dit_linear(const void *a, int64_t lda, const void *w, int64_t ldw,
                       int64_t gate_stride, const int32_t *cu_seqlens, int n_req,
                       dit_dtype dtype, hipStream_t stream);
 
+/* The bf16 GEMM computes 256 x 256 output tiles, or 256 x 192 where fewer
+ * rounds of tiles over the compute units make that faster (shapes with few
+ * tiles).  For tests and tuning: tile_n = 192 or 256 forces that width for
+ * every later bf16 GEMM of this process (every entry point), 0 restores the
+ * choice per shape; any other value gives DIT_ERR_INVALID_ARG.  Results do
+ * not depend on the width.  Process-wide setting; not synchronised with work
+ * in flight (set it between calls). */
+dit_status dit_debug_gemm_tile_n(int tile_n);
+
 /* In place on q and (if not NULL) k, each [rows, n_heads*head_dim] with row
  * stride `row_stride`: per-head RMSNorm with gains g_q / g_k (skipped when the
  * gain is NULL), then, if vl != NULL and the sections are not all 0, the

@@ -154,6 +154,7 @@ def lib() -> ctypes.CDLL:
                                      ctypes.POINTER(ctypes.c_int64)]),
         "dit_migration_execute": (i32, [ctypes.POINTER(CMigField), ctypes.POINTER(CMigEntry), i64,
                                         ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
+        "dit_debug_gemm_tile_n": (i32, [i32]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -173,7 +174,7 @@ def exported_symbols() -> Sequence[str]:
                         "dit_adaln_modulate", "dit_layer_norm_affine", "dit_linear", "dit_qk_norm_rope",
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
                         "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
-                        "dit_migration_plan", "dit_migration_execute",
+                        "dit_migration_plan", "dit_migration_execute", "dit_debug_gemm_tile_n",
                         "dit_status_string",
                         "dit_last_error", "dit_abi_version")]
 
@@ -280,6 +281,11 @@ def block_post_attention(cfg, weights, vl, x, o, txt, mod, y, ws, stream=None, t
                                           _ptr(o), _ptr(txt), _ptr(t), _ptr(mod), _ptr(y), _ptr(ws),
                                           ws.numel() * ws.element_size(), _stream(stream)),
            "dit_block_post_attention")
+
+
+def debug_gemm_tile_n(tile_n: int):
+    """Force the bf16 GEMM's output tile width (192 or 256); 0 restores the choice per shape."""
+    _check(lib().dit_debug_gemm_tile_n(int(tile_n)), "dit_debug_gemm_tile_n")
 
 
 def timestep_modulation(cfg, weights, t, mod, ws, stream=None):

@@ -756,6 +756,14 @@ dit_status dit_timestep_modulation(const dit_block_config* cfg, const dit_block_
   return run_modulation(cfg, w, n_req, t, mod, (char*)ws, stream);
 }
 
+dit_status dit_debug_gemm_tile_n(int tile_n) {
+  g_last_error.clear();
+  if (tile_n != 0 && tile_n != 192 && tile_n != 256)
+    return fail(DIT_ERR_INVALID_ARG, "GEMM tile width %d (0, 192 or 256)", tile_n);
+  set_gemm_tile_n(tile_n);
+  return DIT_OK;
+}
+
 dit_status dit_timestep_modulation_noalloc(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
                                            const float* t, float* mod, hipStream_t stream) {
   g_last_error.clear();

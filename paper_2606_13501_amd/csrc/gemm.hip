@@ -1,9 +1,9 @@
 // Projections of the DiT block: out = epilogue(A . W^T + bias).
 //
-// bf16: a 256x256 output tile per 256-thread workgroup on the gfx950 matrix
-// cores (v_mfma_f32_32x32x16_bf16), fp32 accumulation.  Each of the 4 waves
-// (one per SIMD) owns a 128x128 sub-tile whose accumulators (256 registers)
-// live in the accumulation registers.  The K loop runs in steps of 64: a
+// bf16: a 256x256 (or 256x192) output tile per 256-thread workgroup on the
+// gfx950 matrix cores (v_mfma_f32_32x32x16_bf16), fp32 accumulation.  Each of
+// the 4 waves (one per SIMD) owns a 128x128 (128x96) sub-tile whose
+// accumulators (256 or 192 registers) live in the accumulation registers.  The K loop runs in steps of 64: a
 // step's operand tiles are 256 rows x 128 B, i.e. whole cache lines per row.
 // LDS double-buffers two steps (2 x 64 KiB); two register stages carry the
 // next two steps from global memory, so a load has about two steps of MFMA
@@ -18,6 +18,8 @@
 // resident on one XCD share A and W panels in its L2.
 //
 // fp32: a plain 64x64 LDS-tiled FMA kernel for the small exact configuration.
+#include <atomic>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -25,7 +27,7 @@ namespace dit {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BK = 64;               // tile rows, K step (columns: 256 or 192)
 constexpr int kWaves = 4;                           // 2 x 2 waves, each a 128 x 128 sub-tile
 constexpr int kThreads = 64 * kWaves;
 constexpr int kStages = 2;                          // LDS double buffer
@@ -118,19 +120,24 @@ __device__ __forceinline__ void load_lds16(const u32x4& desc, int voff, int soff
 
 // SEQ: the workgroup runs a sequence of tiles (K / 64 even and >= 6);
 // otherwise one tile per workgroup and any K / 64.
-template <int EPI, bool SEQ>
+template <int EPI, bool SEQ, int BNT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     const bf16* __restrict__ A, int64_t lda, const bf16* __restrict__ W, int64_t ldw,
     const bf16* __restrict__ bias, bf16* __restrict__ C, int64_t ldc, const bf16* R, int64_t ldr,
     const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K,
     int tiles_m, int tiles_n, int plane_cols, int64_t plane_skip) {
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes + kWaves * kEpiBytes];
+  constexpr int WN = BNT / 2;                    // columns of a wave's sub-tile
+  constexpr int NI = WN / 32;                    // its W blocks of 32 columns (4 or 3)
+  constexpr int kTileW = BNT * kRowBytes;        // the W tile of one step
+  constexpr int kStage = kTileBytes + kTileW;    // A tile, then W tile
+  constexpr int kLW = kTileW / 1024 / kWaves;    // 1 KiB W loads per wave and step (8 or 6)
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStage + kWaves * kEpiBytes];
 
   const TileSeq seq = tile_seq(blockIdx.x, gridDim.x, tiles_m, tiles_n);
   if (seq.count == 0) return;
   int tm, tn;
   seq.coords(0, tm, tn);
-  int m0 = tm * BM, n0 = tn * BN;
+  int m0 = tm * BM, n0 = tn * BNT;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -161,23 +168,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // load).  Steps past the last K step (prologue loads of a short K) reload
   // the last one.
   auto a_po = [&](int u) { return (kLoads * wave + u) * 16 * (int)lda; };   // 8 q rows, in bytes
-  auto w_po = [&](int u) { return (kLoads * wave + u) * 16 * (int)ldw; };
+  auto w_po = [&](int u) { return (kLW * wave + u) * 16 * (int)ldw; };
   auto k_off = [&](int step) { return min(step, K / BK - 1) * BK * 2; };
-  struct Stage { u32x4 a[kLoads], w[kLoads]; };   // one step of this wave's pieces
+  struct Stage { u32x4 a[kLoads], w[kLW]; };   // one step of this wave's pieces
   auto gload = [&](Stage& r, int step) {
     const int soff = k_off(step);
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
       r.a[u] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[u & 1] + a_po(u), soff, 0);
-      r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[u & 1] + w_po(u), soff, 0);
+      if (u < kLW) r.w[u] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[u & 1] + w_po(u), soff, 0);
     }
   };
+  // LDS homes of this wave's pieces in the slot of `step`: A piece u, W piece u
+  auto a_home = [&](int step) { return smem + (step % kStages) * kStage + kLoads * wave * 1024 + lane * 16; };
+  auto w_home = [&](int step) {
+    return smem + (step % kStages) * kStage + kTileBytes + kLW * wave * 1024 + lane * 16;
+  };
   auto sstore = [&](const Stage& r, int step) {
-    char* st = smem + (step % kStages) * kStageBytes + kLoads * wave * 1024 + lane * 16;
+    char* const sa = a_home(step);
+    char* const sw = w_home(step);
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      *reinterpret_cast<u32x4*>(st + u * 1024) = r.a[u];
-      *reinterpret_cast<u32x4*>(st + kTileBytes + u * 1024) = r.w[u];
+      *reinterpret_cast<u32x4*>(sa + u * 1024) = r.a[u];
+      if (u < kLW) *reinterpret_cast<u32x4*>(sw + u * 1024) = r.w[u];
     }
   };
 
@@ -189,26 +202,26 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
     fo_a[kk] = (wm * 128 + fr) * kRowBytes + (((2 * kk + fh) ^ sw) << 4);
-    fo_w[kk] = kTileBytes + (wn * 128 + fr) * kRowBytes + (((2 * kk + fh) ^ sw) << 4);
+    fo_w[kk] = kTileBytes + (wn * WN + fr) * kRowBytes + (((2 * kk + fh) ^ sw) << 4);
   }
-  struct Frags { bf16x8 w[4], a[4]; };
+  struct Frags { bf16x8 w[NI], a[4]; };
   auto read = [&](Frags& f, int step, int kk) {
-    const char* st = smem + (step % kStages) * kStageBytes;
+    const char* st = smem + (step % kStages) * kStage;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f.w[i] = *reinterpret_cast<const bf16x8*>(st + fo_w[kk] + i * 32 * kRowBytes);
+    for (int i = 0; i < NI; ++i) f.w[i] = *reinterpret_cast<const bf16x8*>(st + fo_w[kk] + i * 32 * kRowBytes);
 #pragma unroll
     for (int j = 0; j < 4; ++j) f.a[j] = *reinterpret_cast<const bf16x8*>(st + fo_a[kk] + j * 32 * kRowBytes);
   };
 
-  // acc[i][j]: W block i (4 x 32 columns of the wave), A block j (4 x 32 rows)
-  f32x16 acc[4][4];
+  // acc[i][j]: W block i (NI x 32 columns of the wave), A block j (4 x 32 rows)
+  f32x16 acc[NI][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
   auto mma = [&](const Frags& f) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[i], f.a[j], acc[i][j], 0, 0, 0);
@@ -218,33 +231,49 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // is being cycled) 4 LDS stores + 4 global loads, spread evenly: per 4
   // MFMAs 2 reads, 1 store and 1 load.  An even stream of global loads keeps
   // the memory pipeline busy without bursts that would stall MFMA issue.
+  // (With 3 W blocks per wave: 12 MFMAs, 7 reads, up to 4 stores and 4 loads
+  // per quarter, as MFMA, read, MFMA, store, MFMA, read (not in the last
+  // group), load.)
   auto pattern = [] {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if constexpr (NI == 4) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
     }
   };
   // items u0 .. u0 + 3 of a register stage (items 0-7: A pieces, 8-15: W
   // pieces): store each into the LDS slot of step st_step, then reload it
   // with step ld_step (each part only when asked for)
   auto io4 = [&](Stage& R, int u0, int st_step, int ld_step, bool do_store, bool do_load) {
-    char* st = smem + (st_step % kStages) * kStageBytes + kLoads * wave * 1024 + lane * 16;
+    char* const sa = a_home(st_step);
+    char* const sw = w_home(st_step);
     const int soff = ld_step * BK * 2;   // loads are asked for only while ld_step < K / 64
 #pragma unroll
     for (int u = u0; u < u0 + 4; ++u) {
       const int p = u & 7;
-      u32x4& v = u < 8 ? R.a[p] : R.w[p];
-      if (do_store) *reinterpret_cast<u32x4*>(st + (u < 8 ? 0 : kTileBytes) + p * 1024) = v;
-      if (do_load)
-        v = u < 8 ? __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[p & 1] + a_po(p), soff, 0)
-                  : __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[p & 1] + w_po(p), soff, 0);
+      if (u < 8) {
+        if (do_store) *reinterpret_cast<u32x4*>(sa + p * 1024) = R.a[p];
+        if (do_load) R.a[p] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, a_vo[p & 1] + a_po(p), soff, 0);
+      } else if (p < kLW) {
+        if (do_store) *reinterpret_cast<u32x4*>(sw + p * 1024) = R.w[p];
+        if (do_load) R.w[p] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, w_vo[p & 1] + w_po(p), soff, 0);
+      }
     }
   };
 
@@ -273,12 +302,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   u32x4 nad{}, nwd{};   // the next tile's A and W
   bool has_next = false;
   auto dma_step = [&](int step) {   // step 0 or 1 of the next tile into slot `step` (K / 64 >= 6 here)
-    const uint32_t st = lds_base + step * kStageBytes + kLoads * wave * 1024;
+    const uint32_t sa = lds_base + step * kStage + kLoads * wave * 1024;
+    const uint32_t sw = lds_base + step * kStage + kTileBytes + kLW * wave * 1024;
     const int soff = step * BK * 2;
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      load_lds16(nad, a_vo[u & 1] + a_po(u), soff, st + u * 1024);
-      load_lds16(nwd, w_vo[u & 1] + w_po(u), soff, st + kTileBytes + u * 1024);
+      load_lds16(nad, a_vo[u & 1] + a_po(u), soff, sa + u * 1024);
+      if (u < kLW) load_lds16(nwd, w_vo[u & 1] + w_po(u), soff, sw + u * 1024);
     }
   };
   Stage r0, r1;
@@ -321,7 +351,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     if (has_next) {
       seq.coords(it + 1, tm1, tn1);
       nad = make_desc(A + (int64_t)tm1 * BM * lda, ((int64_t)(M - tm1 * BM - 1) * lda + K) * 2);
-      nwd = make_desc(W + (int64_t)tn1 * BN * ldw, ((int64_t)(N - tn1 * BN - 1) * ldw + K) * 2);
+      nwd = make_desc(W + (int64_t)tn1 * BNT * ldw, ((int64_t)(N - tn1 * BNT - 1) * ldw + K) * 2);
     }
     // r0 / r1 carry steps 2 / 3; keep the two register stages' loads in this
     // order (as in the loop), so the wait counts the compiler derives inside
@@ -371,17 +401,17 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   // outputs is computed, so the epilogue waits for memory twice per tile;
   // the register stages are free here.  C may alias R: every element is
   // read before it is written, by the same lane.
-  char* const ew = smem + kStages * kStageBytes + wave * kEpiBytes;
+  char* const ew = smem + kStages * kStage + wave * kEpiBytes;
   const int er = lane >> 4, ec = lane & 15;   // read role: rows er + 4 k, chunk ec
   float bsum[2][4];
   int64_t c_off[2];   // output plane of the lane's 4 columns (planes: column n in plane n / plane_cols)
 #pragma unroll
   for (int ih = 0; ih < 2; ++ih) {
-    const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+    const int n = n0 + wn * WN + 64 * ih + 4 * ec;
     c_off[ih] = plane_cols > 0 ? (int64_t)(n / plane_cols) * plane_skip : 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) bsum[ih][e] = 0.f;
-    if (bias && n < N) {
+    if (bias && n < N && 64 * ih + 4 * ec < WN) {
       const bf16x4 bv = *reinterpret_cast<const bf16x4*>(bias + n);
 #pragma unroll
       for (int e = 0; e < 4; ++e) bsum[ih][e] = (float)bv[e];
@@ -402,20 +432,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
         g_one[jj] = r_lo == r_hi;
 #pragma unroll
         for (int ih = 0; ih < 2; ++ih) {
-          const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+          const int n = n0 + wn * WN + 64 * ih + 4 * ec;
           gv[jj][ih] = f32x4{};
-          if (g_one[jj] && n < N) gv[jj][ih] = *reinterpret_cast<const f32x4*>(gate + (int64_t)r_lo * gate_stride + n);
+          if (g_one[jj] && n < N && 64 * ih + 4 * ec < WN)
+            gv[jj][ih] = *reinterpret_cast<const f32x4*>(gate + (int64_t)r_lo * gate_stride + n);
         }
       }
       if (kRes) {
 #pragma unroll
         for (int ih = 0; ih < 2; ++ih) {
-          const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
+          const int n = n0 + wn * WN + 64 * ih + 4 * ec;
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             const int m = mb + 4 * k + er;
             rv[jj][ih][k] = bf16x4{};
-            if (m < M && n < N) rv[jj][ih][k] = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
+            if (m < M && n < N && 64 * ih + 4 * ec < WN)
+              rv[jj][ih][k] = *reinterpret_cast<const bf16x4*>(R + (int64_t)m * ldr + n);
           }
         }
       }
@@ -426,7 +458,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
 #pragma unroll
       for (int ih = 0; ih < 2; ++ih) {
 #pragma unroll
-        for (int ii = 0; ii < 2; ++ii)
+        for (int ii = 0; ii < 2; ++ii) {
+          if (2 * ih + ii >= NI) continue;   // 3 W blocks: the last round holds one block (32 columns)
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
             const f32x4 v = {acc[2 * ih + ii][j][4 * gq], acc[2 * ih + ii][j][4 * gq + 1],
@@ -434,8 +467,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
             const int c = 8 * ii + 2 * gq + fh;
             *reinterpret_cast<f32x4*>(ew + fr * 256 + ((c ^ (fr & 15)) << 4)) = v;
           }
-        const int n = n0 + wn * 128 + 64 * ih + 4 * ec;
-        if (n >= N) continue;
+        }
+        const int n = n0 + wn * WN + 64 * ih + 4 * ec;
+        if (n >= N || 64 * ih + 4 * ec >= WN) continue;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
           const int r = 4 * k + er;
@@ -472,7 +506,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
     m0 = tm1 * BM;
-    n0 = tn1 * BN;
+    n0 = tn1 * BNT;
     a_rs = make_rsrc(A + (int64_t)m0 * lda, ((int64_t)(M - m0 - 1) * lda + K) * 2);
     w_rs = make_rsrc(W + (int64_t)n0 * ldw, ((int64_t)(N - n0 - 1) * ldw + K) * 2);
   }
@@ -549,30 +583,45 @@ int cu_count() {
   return cached[dev];
 }
 
-template <int EPI>
-hipError_t launch_bf16(const LinearArgs& p, hipStream_t s) {
-  int tiles_m = (int)((p.M + BM - 1) / BM);
-  int tiles_n = (p.N + BN - 1) / BN;
-  int tiles = tiles_m * tiles_n;
+std::atomic<int> g_tile_n{0};   // forced output tile width (0: chosen per shape)
+
+template <int EPI, int BNT>
+hipError_t launch_bf16_tiles(const LinearArgs& p, int tiles_m, int tiles_n, hipStream_t s) {
+  const int tiles = tiles_m * tiles_n;
   int grid = (tiles + kXcds - 1) / kXcds * kXcds;   // one tile per workgroup
   const int kt = p.K / BK;
   if (kt % 2 == 0 && kt >= 6) {
     // one workgroup per compute unit, each running a sequence of tiles
     const int resident = cu_count() / kXcds * kXcds;
     if (resident >= kXcds && grid > resident) grid = resident;
-    gemm_bf16_nt<EPI, true><<<grid, kThreads, 0, s>>>(
+    gemm_bf16_nt<EPI, true, BNT><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
         (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
-        p.plane_cols,
-        p.plane_stride - p.plane_cols);
+        p.plane_cols, p.plane_stride - p.plane_cols);
   } else {
-    gemm_bf16_nt<EPI, false><<<grid, kThreads, 0, s>>>(
+    gemm_bf16_nt<EPI, false, BNT><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
         (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
-        p.plane_cols,
-        p.plane_stride - p.plane_cols);
+        p.plane_cols, p.plane_stride - p.plane_cols);
   }
   return hipGetLastError();
+}
+
+// Output tiles are 256 x 256, or 256 x 192 where that needs fewer rounds of
+// tiles over the compute units: with few tiles the last round leaves compute
+// units idle (4,096 rows x 3,072 columns: 192 tiles of 256 x 256 on 256 CUs,
+// but exactly 256 of 256 x 192).  A round of narrow tiles is costed at
+// 192 / 256 of a wide one, plus 8% (7 fragment reads per 12 MFMAs instead of
+// 8 per 16).
+template <int EPI>
+hipError_t launch_bf16(const LinearArgs& p, hipStream_t s) {
+  const int tiles_m = (int)((p.M + BM - 1) / BM);
+  const int cus = cu_count();
+  auto rounds = [&](int bn) { return ((int64_t)tiles_m * ((p.N + bn - 1) / bn) + cus - 1) / cus; };
+  int bn = g_tile_n.load(std::memory_order_relaxed);
+  if (bn != 192 && bn != 256) bn = rounds(192) * 192 * 108 < rounds(256) * 256 * 100 ? 192 : 256;
+  if (bn == 192) return launch_bf16_tiles<EPI, 192>(p, tiles_m, (p.N + 191) / 192, s);
+  return launch_bf16_tiles<EPI, 256>(p, tiles_m, (p.N + 255) / 256, s);
 }
 
 template <int EPI>
@@ -586,6 +635,8 @@ hipError_t launch_f32(const LinearArgs& p, hipStream_t s) {
 }
 
 }  // namespace
+
+void set_gemm_tile_n(int bn) { g_tile_n.store(bn, std::memory_order_relaxed); }
 
 hipError_t launch_linear(const LinearArgs& p, hipStream_t s) {
   if (p.M == 0) return hipSuccess;

@@ -28,6 +28,8 @@ struct LinearArgs {
   int64_t plane_stride = 0;
 };
 hipError_t launch_linear(const LinearArgs& p, hipStream_t s);
+// Forces the bf16 GEMM's output tile width (192 or 256; 0: chosen per shape).
+void set_gemm_tile_n(int bn);
 
 struct AttnArgs {
   const void *q, *k, *v;

@@ -125,6 +125,15 @@ def test_linear_rejects_bad_arguments():
     assert f(P, 128, 12, 64, 128, 9, None, None, None, 0, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
 
 
+def test_gemm_tile_width_hook():
+    L = _lib()
+    for bad in (1, 128, 200, -1, 512):
+        assert L.dit_debug_gemm_tile_n(bad) == B.DIT_ERR_INVALID_ARG
+        assert b"tile width" in L.dit_last_error()
+    for good in (192, 256, 0):   # ends on 0: the per-shape choice
+        assert L.dit_debug_gemm_tile_n(good) == B.DIT_OK
+
+
 def test_norm_kernels_reject_bad_arguments():
     L = _lib()
     S = ctypes.c_void_p(0)

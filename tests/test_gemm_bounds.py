@@ -16,12 +16,15 @@ import pytest
 BM, BK, WAVES, LOADS = 256, 64, 4, 8
 
 
-def load_extents(M, K, ld, row_in_lane=True):
+def load_extents(M, K, ld, row_in_lane=True, tile=BM, loads=LOADS):
     """(lowest, highest) byte touched by the loads of every tile, relative to
     the operand's base, for all K steps the kernel issues (0 .. max(K/64, 4)).
+    tile / loads: rows of the operand's tile and 1 KiB loads per wave (A: 256
+    and 8; W: 256 and 8, or 192 and 6 for the narrow tiles).
     row_in_lane=False models the earlier layout (piece row in the scalar
     offset, outside the range check)."""
-    tiles = (M + BM - 1) // BM
+    assert tile == 8 * loads * WAVES
+    tiles = (M + tile - 1) // tile
     kt = K // BK
     lane = np.arange(64)
     lo, hi = np.inf, -np.inf
@@ -29,11 +32,11 @@ def load_extents(M, K, ld, row_in_lane=True):
     # past the last one reloads the last one
     steps = np.minimum(np.arange(max(kt, 4)), kt - 1) * BK * 2
     for tm in range(tiles):
-        m0 = tm * BM
+        m0 = tm * tile
         n_rec = ((M - m0 - 1) * ld + K) * 2
         for wave in range(WAVES):
-            for u in range(LOADS):
-                q = LOADS * wave + u
+            for u in range(loads):
+                q = loads * wave + u
                 c = (lane & 7) ^ (4 * (q & 1) + (lane >> 4))
                 lane_part = (lane >> 3) * ld * 2 + c * 16
                 piece = 8 * q * ld * 2
@@ -69,3 +72,59 @@ def test_scalar_piece_offset_would_leave_the_operand():
     M, K, ld = 75600, 5120, 5120
     lo, hi = load_extents(M, K, ld, row_in_lane=False)
     assert hi > ((M - 1) * ld + K) * 2 - 1
+
+
+@pytest.mark.parametrize("N,K,ld", [
+    (3072, 3072, 3072),      # image block: O, cross-Q, cross-O weights (16 narrow tiles)
+    (9216, 3072, 3072),      # image block QKV weight
+    (6144, 3072, 3072),      # image block text key/value weight
+    (264, 64, 64),           # ragged: 2 narrow tiles, the second with 72 rows
+    (2880, 768, 768),        # ragged, the tile-sequence test's weight
+    (8, 128, 128),           # fewer rows than one load piece
+])
+def test_gemm_narrow_tile_weight_loads_stay_inside_operand(N, K, ld):
+    lo, hi = load_extents(N, K, ld, tile=192, loads=6)
+    last = ((N - 1) * ld + K) * 2 - 1
+    assert lo >= 0
+    assert hi <= last, f"a load reaches byte {hi}, past the operand's last byte {last}"
+
+
+def lds_extent(bnt):
+    """Highest LDS byte each kind of access of the bf16 GEMM touches, for
+    output tiles of 256 x bnt, and the size of the kernel's LDS array."""
+    row_bytes, stages, epi = BK * 2, 2, 32 * 256
+    tile_a, tile_w = BM * row_bytes, bnt * row_bytes
+    stage = tile_a + tile_w
+    kla, klw = tile_a // 1024 // WAVES, tile_w // 1024 // WAVES
+    wn, ni = bnt // 2, bnt // 64
+    total = stages * stage + WAVES * epi
+    hi = {}
+    lane = np.arange(64)
+    for step in range(stages):
+        for wave in range(WAVES):
+            a_home = step * stage + kla * wave * 1024 + lane * 16
+            w_home = step * stage + tile_a + klw * wave * 1024 + lane * 16
+            hi["store A"] = max(hi.get("store A", 0), (a_home + (kla - 1) * 1024).max() + 15)
+            hi["store W"] = max(hi.get("store W", 0), (w_home + (klw - 1) * 1024).max() + 15)
+            wm, wnn = wave >> 1, wave & 1
+            fr, fh = lane & 31, lane >> 5
+            sw = (fr >> 1) & 7
+            for kk in range(4):
+                fo_a = (wm * 128 + fr) * row_bytes + (((2 * kk + fh) ^ sw) << 4)
+                fo_w = tile_a + (wnn * wn + fr) * row_bytes + (((2 * kk + fh) ^ sw) << 4)
+                hi["read A"] = max(hi.get("read A", 0), (step * stage + fo_a + 3 * 32 * row_bytes).max() + 15)
+                hi["read W"] = max(hi.get("read W", 0), (step * stage + fo_w + (ni - 1) * 32 * row_bytes).max() + 15)
+            # A and W regions of a slot stay apart
+            assert (a_home + (kla - 1) * 1024).max() + 15 < step * stage + tile_a
+            assert (w_home + (klw - 1) * 1024).max() + 15 < (step + 1) * stage
+    for wave in range(WAVES):
+        hi["epilogue"] = max(hi.get("epilogue", 0), stages * stage + wave * epi + epi - 1)
+    return hi, total
+
+
+@pytest.mark.parametrize("bnt", [256, 192])
+def test_gemm_lds_accesses_stay_inside_the_array(bnt):
+    hi, total = lds_extent(bnt)
+    for kind, h in hi.items():
+        assert h < total, f"{kind} reaches LDS byte {h} of {total}"
+    assert total <= 160 * 1024

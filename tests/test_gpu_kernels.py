@@ -69,22 +69,32 @@ GEMM_CASES = [
 ]
 
 
+class forced_tile_n:
+    """Force the bf16 GEMM's output tile width (192 or 256) inside a with-block;
+    0 (the per-shape choice) again afterwards."""
+
+    def __init__(self, B, tile_n):
+        self.B, self.tile_n = B, tile_n
+
+    def __enter__(self):
+        self.B.debug_gemm_tile_n(self.tile_n)
+
+    def __exit__(self, *exc):
+        self.B.debug_gemm_tile_n(0)
+
+
 @pytest.mark.parametrize("dtype,M,N,K,lengths", GEMM_CASES)
 @pytest.mark.parametrize("epi", [0, 1, 2, 3])
 def test_linear(dtype, M, N, K, lengths, epi):
+    """bf16: both output tile widths (256 and 192 columns), each against the oracle."""
     B = require_gpu()
-    log(f"case linear {dtype} M={M} N={N} K={K} epi={epi} lengths={lengths}")
     cu = _cu(lengths)
     a = synth.draw((M, K), (10, M, N, K), dtype)
     w = synth.draw((N, K), (11, M, N, K), dtype, std=0.02)
     b = synth.draw((N,), (12, M, N, K), dtype, std=0.02)
     res = synth.draw((M, N), (13, M, N, K), dtype)
     gate = synth.draw((len(lengths), 2 * N), (14, M, N, K), "f32", std=0.7)
-    out = empty((M, N), dtype)
     gt = dev(gate)
-    B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
-             gate=gt[:, N:] if epi == 3 else None, gate_stride=2 * N, cu_seqlens=cu if epi == 3 else None)
-    torch.cuda.synchronize()
     z = O.linear(O.decode(a), O.decode(w), O.decode(b))
     if epi == 1:
         z = O.gelu_tanh(z)
@@ -92,7 +102,14 @@ def test_linear(dtype, M, N, K, lengths, epi):
         z = O.decode(res) + z
     elif epi == 3:
         z = O.decode(res) + gate[_req_of(cu), N:].astype(np.float64) * z
-    check(host(out), z, dtype, f"linear epi={epi}")
+    for tile_n in ((256, 192) if dtype == "bf16" else (0,)):
+        log(f"case linear {dtype} M={M} N={N} K={K} epi={epi} lengths={lengths} tile_n={tile_n}")
+        out = empty((M, N), dtype)
+        with forced_tile_n(B, tile_n):
+            B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
+                     gate=gt[:, N:] if epi == 3 else None, gate_stride=2 * N, cu_seqlens=cu if epi == 3 else None)
+            torch.cuda.synchronize()
+        check(host(out), z, dtype, f"linear epi={epi} tile_n={tile_n}")
 
 
 @pytest.mark.parametrize("epi", [0, 1, 3])
@@ -103,17 +120,12 @@ def test_linear_tile_sequences(epi):
     covering the first, middle and last row of every tile row."""
     B = require_gpu()
     M, N, K, lengths = 12288 + 77, 2816 + 64, 768, [5000, 7365]
-    log(f"case linear tile sequences M={M} N={N} K={K} epi={epi}")
     cu = _cu(lengths)
     a = synth.draw((M, K), (15, M, N, K), "bf16")
     w = synth.draw((N, K), (16, M, N, K), "bf16", std=0.02)
     b = synth.draw((N,), (17, M, N, K), "bf16", std=0.02)
     res = synth.draw((M, N), (18, M, N, K), "bf16")
     gate = synth.draw((len(lengths), N), (19, M, N, K), "f32", std=0.7)
-    out = empty((M, N), "bf16")
-    B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
-             gate=dev(gate) if epi == 3 else None, gate_stride=N, cu_seqlens=cu if epi == 3 else None)
-    torch.cuda.synchronize()
     rows = np.unique(np.concatenate([np.arange(0, M, 256), np.minimum(np.arange(0, M, 256) + 128, M - 1),
                                      np.minimum(np.arange(0, M, 256) + 255, M - 1), [M - 1],
                                      np.random.default_rng(7).integers(0, M, 200)]))
@@ -122,7 +134,14 @@ def test_linear_tile_sequences(epi):
         z = O.gelu_tanh(z)
     elif epi == 3:
         z = O.decode(res[rows]) + gate[_req_of(cu)[rows]].astype(np.float64) * z
-    check(host(out)[rows], z, "bf16", f"linear tile sequences epi={epi}")
+    for tile_n in (256, 192):   # 49 x 12 or 49 x 15 tiles (the last column tile ragged in both)
+        log(f"case linear tile sequences M={M} N={N} K={K} epi={epi} tile_n={tile_n}")
+        out = empty((M, N), "bf16")
+        with forced_tile_n(B, tile_n):
+            B.linear(dev(a), dev(w), dev(b), out, epi=epi, res=dev(res) if epi >= 2 else None,
+                     gate=dev(gate) if epi == 3 else None, gate_stride=N, cu_seqlens=cu if epi == 3 else None)
+            torch.cuda.synchronize()
+        check(host(out)[rows], z, "bf16", f"linear tile sequences epi={epi} tile_n={tile_n}")
 
 
 def test_linear_inplace_residual():
