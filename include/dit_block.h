@@ -237,6 +237,19 @@ dit_status dit_linear(const void *a, int64_t lda, const void *w, int64_t ldw,
  * in flight (set it between calls). */
 dit_status dit_debug_gemm_tile_n(int tile_n);
 
+/* The bf16 self-attention (key ranges over 1024) runs its work items in
+ * rounds of one workgroup per compute unit.  When the last round would be at
+ * most half full (one request), its items are split into 2 or 4 key pieces
+ * that run as one short round and are merged by a second kernel; the pieces
+ * live in a static device array of 34 MB that every GPU holds until the
+ * process ends, and calls that split are serialised on it by an event (not
+ * under graph capture, where no split happens).  For tests and tuning:
+ * mode 2 or 4 forces a split of the last request's last items (as many as
+ * one round of pieces holds) into that many pieces, 1 disables splitting,
+ * 0 restores the choice per shape; other values give DIT_ERR_INVALID_ARG.
+ * Process-wide; set it between calls. */
+dit_status dit_debug_attention_split(int mode);
+
 /* In place on q and (if not NULL) k, each [rows, n_heads*head_dim] with row
  * stride `row_stride`: per-head RMSNorm with gains g_q / g_k (skipped when the
  * gain is NULL), then, if vl != NULL and the sections are not all 0, the

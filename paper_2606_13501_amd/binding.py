@@ -155,6 +155,7 @@ def lib() -> ctypes.CDLL:
         "dit_migration_execute": (i32, [ctypes.POINTER(CMigField), ctypes.POINTER(CMigEntry), i64,
                                         ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
         "dit_debug_gemm_tile_n": (i32, [i32]),
+        "dit_debug_attention_split": (i32, [i32]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -175,6 +176,7 @@ def exported_symbols() -> Sequence[str]:
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
                         "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
                         "dit_migration_plan", "dit_migration_execute", "dit_debug_gemm_tile_n",
+                        "dit_debug_attention_split",
                         "dit_status_string",
                         "dit_last_error", "dit_abi_version")]
 
@@ -286,6 +288,11 @@ def block_post_attention(cfg, weights, vl, x, o, txt, mod, y, ws, stream=None, t
 def debug_gemm_tile_n(tile_n: int):
     """Force the bf16 GEMM's output tile width (192 or 256); 0 restores the choice per shape."""
     _check(lib().dit_debug_gemm_tile_n(int(tile_n)), "dit_debug_gemm_tile_n")
+
+
+def debug_attention_split(mode: int):
+    """bf16 self-attention's split of its last round: 2 or 4 forces that many key pieces, 1 never, 0 per shape."""
+    _check(lib().dit_debug_attention_split(int(mode)), "dit_debug_attention_split")
 
 
 def timestep_modulation(cfg, weights, t, mod, ws, stream=None):

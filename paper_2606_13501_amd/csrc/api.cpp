@@ -764,6 +764,14 @@ dit_status dit_debug_gemm_tile_n(int tile_n) {
   return DIT_OK;
 }
 
+dit_status dit_debug_attention_split(int mode) {
+  g_last_error.clear();
+  if (mode != 0 && mode != 1 && mode != 2 && mode != 4)
+    return fail(DIT_ERR_INVALID_ARG, "attention split mode %d (0, 1, 2 or 4)", mode);
+  set_attention_split(mode);
+  return DIT_OK;
+}
+
 dit_status dit_timestep_modulation_noalloc(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
                                            const float* t, float* mod, hipStream_t stream) {
   g_last_error.clear();

@@ -33,6 +33,9 @@
 //
 // fp32: one thread per (query row, head) with an exact online softmax.
 #include <float.h>
+
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -66,6 +69,13 @@ struct AttnWork {
   int k_len[DIT_MAX_REQ];
   int tiles_q[DIT_MAX_REQ];         // query tiles of one head
   int prefix[DIT_MAX_REQ + 1];      // work items before request i (all heads)
+  // Split items (split_s > 0): workgroup split_base + b computes key piece
+  // b % split_s of item split_first + b / split_s of request split_req (the
+  // first split_first items of that request are whole items) and writes its
+  // unnormalised output, row reference and row sum to part, for split_n
+  // pieces in all (see the launcher)
+  int split_s, split_req, split_first, split_base, split_n;
+  float* part;
 };
 
 // Raw buffer descriptor over `bytes` bytes from `base`: loads past the end
@@ -134,25 +144,39 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
   // the same contiguous eighth of every request's items (head-major, requests
   // longest first): the long requests' work is spread over all XCDs, and the
   // query tiles of one head stay together on one XCD, sharing its K/V in L2.
-  const int xcd = blockIdx.x % kXcds;
-  int j = blockIdx.x / kXcds;
-  int r = 0, local = -1;
-  for (; r < work.n_req; ++r) {
-    const int n_r = work.prefix[r + 1] - work.prefix[r];
-    const int lo = xcd * n_r / kXcds, hi = (xcd + 1) * n_r / kXcds;
-    if (j < hi - lo) {
-      local = lo + j;
-      break;
+  int r = 0, local = -1, piece = -1;
+  if (work.split_s > 0 && (int)blockIdx.x >= work.split_base) {
+    const int b = (int)blockIdx.x - work.split_base;
+    r = work.split_req;
+    local = work.split_first + b / work.split_s;
+    piece = b % work.split_s;
+  } else {
+    const int xcd = blockIdx.x % kXcds;
+    int j = blockIdx.x / kXcds;
+    for (; r < work.n_req; ++r) {
+      const int n_r = work.prefix[r + 1] - work.prefix[r];
+      const int lo = xcd * n_r / kXcds, hi = (xcd + 1) * n_r / kXcds;
+      if (j < hi - lo) {
+        local = lo + j;
+        break;
+      }
+      j -= hi - lo;
     }
-    j -= hi - lo;
+    if (local < 0) return;
   }
-  if (local < 0) return;
   const int head = local / work.tiles_q[r];
   const int qt = local - head * work.tiles_q[r];
   const int q0 = work.q_start[r] + qt * BQ;
   const int q_end = work.q_start[r] + work.q_len[r];
-  const int k0 = work.k_start[r];
-  const int n_k = work.k_len[r];
+  int k0 = work.k_start[r];
+  int n_k = work.k_len[r];
+  if (piece >= 0) {   // this piece's key tiles: a contiguous 1 / split_s of the request's
+    const int kt_all = (n_k + BKV - 1) / BKV;
+    const int per = (kt_all + work.split_s - 1) / work.split_s;
+    const int kt0 = min(piece * per, kt_all);
+    k0 += kt0 * BKV;
+    n_k = max(0, min(n_k - kt0 * BKV, per * BKV));
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -430,6 +454,25 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
 
   // ---- normalise and store
   const float l_tot = row_sum();
+  if (piece >= 0) {
+    // a piece: its unnormalised output (fp32), and the row's reference and
+    // sum, for the merge kernel; rows past the request are written too (the
+    // merge skips them)
+    const int row = ((int)blockIdx.x - work.split_base) * BQ + 32 * wave + fr;
+    float* po = work.part + (int64_t)row * D + 4 * fh;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<f32x4*>(po + 32 * db + 8 * i) =
+            f32x4{oacc[db][4 * i], oacc[db][4 * i + 1], oacc[db][4 * i + 2], oacc[db][4 * i + 3]};
+    if (fh == 0) {
+      float* pm = work.part + (int64_t)work.split_n * BQ * D + 2 * (int64_t)row;
+      pm[0] = m_ref;
+      pm[1] = l_tot;
+    }
+    return;
+  }
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
   if (my_q < q_end) {
     bf16* op = O + (int64_t)my_q * os + head * D + 4 * fh;
@@ -443,6 +486,49 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
         *reinterpret_cast<bf16x4*>(op + 32 * db + 8 * i) = ov;
       }
   }
+}
+
+// Merge of split items (256-query pieces of the 8-wave shape): row q of item
+// it gets O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p over the pieces p
+// that had keys (l_p > 0), with m their largest reference; O_p, m_p, l_p as
+// the pieces wrote them (P = 2^(score - m_p), in log2 units).  One wave per
+// row, two columns per lane.
+__global__ __launch_bounds__(256) void attn_merge_kernel(bf16* __restrict__ O, int64_t os, const float* part,
+                                                         int n_pieces, AttnWork work) {
+  constexpr int BQ = 256;
+  const int row = (int)blockIdx.x * 4 + (threadIdx.x >> 6);   // split item it, row rl
+  const int lane = threadIdx.x & 63;
+  const int S = work.split_s;
+  const int it = row / BQ, rl = row - it * BQ;
+  if (it >= n_pieces / S) return;
+  const int r = work.split_req;
+  const int local = work.split_first + it;
+  const int head = local / work.tiles_q[r];
+  const int qt = local - head * work.tiles_q[r];
+  const int q = work.q_start[r] + qt * BQ + rl;
+  if (q >= work.q_start[r] + work.q_len[r]) return;
+  const float* ml = part + (int64_t)n_pieces * BQ * D;
+  float m = -INFINITY;
+  for (int p = 0; p < S; ++p) {
+    const int64_t idx = (int64_t)(it * S + p) * BQ + rl;
+    if (ml[2 * idx + 1] > 0.f) m = fmaxf(m, ml[2 * idx]);
+  }
+  float l = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int p = 0; p < S; ++p) {
+    const int64_t idx = (int64_t)(it * S + p) * BQ + rl;
+    const float lp = ml[2 * idx + 1];
+    if (!(lp > 0.f)) continue;
+    const float wp = exp2f(ml[2 * idx] - m);
+    const float2 v = *reinterpret_cast<const float2*>(part + idx * D + 2 * lane);
+    l = fmaf(wp, lp, l);
+    o0 = fmaf(wp, v.x, o0);
+    o1 = fmaf(wp, v.y, o1);
+  }
+  const float inv = l > 0.f ? 1.0f / l : 0.f;
+  bf16x2 ov;
+  ov[0] = (bf16)(o0 * inv);
+  ov[1] = (bf16)(o1 * inv);
+  *reinterpret_cast<bf16x2*>(O + (int64_t)q * os + head * D + 2 * lane) = ov;
 }
 
 // ------------------------------------------------------------------- fp32
@@ -500,6 +586,93 @@ __global__ __launch_bounds__(64) void attn_fwd_f32(
 
 }  // namespace
 
+// Pieces of split work items (see launch_attention): at most kMaxPieces
+// pieces of 256 rows, each its fp32 output [256][128], then the rows'
+// reference and sum [256][2].  One array per GPU, held until the process
+// ends; calls that split are serialised on it by an event (below).
+constexpr int kMaxPieces = 256;
+static __device__ __align__(256) float attn_part[kMaxPieces * (256 * D + 2 * 256)];
+
+namespace {
+
+std::atomic<int> g_split_mode{0};   // 0 per shape, 1 never, 2 or 4 forced
+
+struct SplitState {
+  std::mutex mu;               // a call's enqueue from the event wait to the event record
+  hipEvent_t done = nullptr;   // recorded after the last merge that read attn_part
+  float* part = nullptr;       // device address of this GPU's attn_part
+  bool used = false;
+};
+
+// This device's split state, created on first use (NULL if it cannot be).
+SplitState* split_state() {
+  static std::mutex mu;
+  static SplitState* st[64] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!st[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(attn_part)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    SplitState* x = new SplitState;
+    x->part = (float*)ptr;
+    if (hipEventCreateWithFlags(&x->done, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      delete x;
+      return nullptr;
+    }
+    st[dev] = x;
+  }
+  return st[dev];
+}
+
+struct Split {
+  int s = 0;   // key pieces per split item (0: no split)
+  int n = 0;   // split items: the last request's last n
+};
+
+// A launch runs its items in rounds of one workgroup per compute unit.  When
+// the last round is at most half full (a single request; at 720p 11,840 items
+// on 256 CUs leave 64 for a 47th round), those items are split into 2 or 4
+// key pieces, so the last round is 1/2 or 1/4 as long.  Not under graph
+// capture (the split serialises calls through an event recorded outside it).
+Split choose_split(const AttnWork& w, hipStream_t s) {
+  Split sp;
+  const int mode = g_split_mode.load(std::memory_order_relaxed);
+  if (mode == 1 || w.n_req < 1) return sp;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    return sp;
+  }
+  const int n = w.n_req, last = n - 1;
+  const int items = w.prefix[n], items_last = w.prefix[n] - w.prefix[last];
+  const int kt_last = (w.k_len[last] + BKV - 1) / BKV;
+  const int slots = cu_count();
+  if (mode == 2 || mode == 4) {
+    sp.s = mode;
+    sp.n = min(items_last, slots / mode);
+  } else if (n == 1) {
+    const int rounds = (items + slots - 1) / slots;
+    const int left = items - (rounds - 1) * slots;
+    if (rounds >= 2 && left <= slots / 2) {
+      sp.s = left <= slots / 4 ? 4 : 2;
+      sp.n = left;
+    }
+  }
+  if (sp.s == 0 || sp.n < 1 || sp.n > items_last || kt_last < 8 * sp.s || sp.n * sp.s > kMaxPieces ||
+      !split_state())
+    return Split{};
+  return sp;
+}
+
+}  // namespace
+
+void set_attention_split(int mode) { g_split_mode.store(mode, std::memory_order_relaxed); }
+
 hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
   const int n_req = p.cq.n_req;
   if (p.dtype == DIT_F32) {
@@ -548,28 +721,64 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
   if (items == 0) return hipSuccess;
   if (items > (1 << 27)) return hipErrorInvalidValue;   // keeps (xcd + 1) * n_r in range
   // each XCD's share of every request (see the kernel); the grid covers the largest
-  int per_xcd = 0;
-  for (int x = 0; x < kXcds; ++x) {
-    int len = 0;
-    for (int i = 0; i < n; ++i) {
-      const int n_r = w.prefix[i + 1] - w.prefix[i];
-      len += (x + 1) * n_r / kXcds - x * n_r / kXcds;
+  auto grid_of = [](const AttnWork& wk) {
+    int per_xcd = 0;
+    for (int x = 0; x < kXcds; ++x) {
+      int len = 0;
+      for (int i = 0; i < wk.n_req; ++i) {
+        const int n_r = wk.prefix[i + 1] - wk.prefix[i];
+        len += (x + 1) * n_r / kXcds - x * n_r / kXcds;
+      }
+      per_xcd = len > per_xcd ? len : per_xcd;
     }
-    per_xcd = len > per_xcd ? len : per_xcd;
-  }
-  const int grid = per_xcd * kXcds;
+    return per_xcd * kXcds;
+  };
   const float scale_log2 = p.scale * 1.4426950408889634f;
   const bf16* g = (const bf16*)p.q_gain;
+  auto launch = [&](const AttnWork& wk, int grid) {
+    if (grid <= 0) return;
 #define DIT_ATTN_ARGS                                                                                          \
   (const bf16*)p.q, (const bf16*)p.k, (const bf16*)p.v, (bf16*)p.o, p.q_stride, p.k_stride, p.v_stride,        \
-      p.o_stride, p.n_heads, scale_log2, g, p.q_eps, w
-  if (short_keys) {
-    if (g) attn_fwd_bf16<4, 2, true><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
-    else attn_fwd_bf16<4, 2, false><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
-  } else {
-    if (g) attn_fwd_bf16<8, 4, true><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
-    else attn_fwd_bf16<8, 4, false><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
+      p.o_stride, p.n_heads, scale_log2, g, p.q_eps, wk
+    if (short_keys) {
+      if (g) attn_fwd_bf16<4, 2, true><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
+      else attn_fwd_bf16<4, 2, false><<<grid, 256, 0, s>>>(DIT_ATTN_ARGS);
+    } else {
+      if (g) attn_fwd_bf16<8, 4, true><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
+      else attn_fwd_bf16<8, 4, false><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
+    }
+  };
+  const Split sp = short_keys ? Split{} : choose_split(w, s);
+  if (sp.s == 0) {
+    launch(w, grid_of(w));
+    return hipGetLastError();
   }
+  // The last request's last n_split items as `split` key pieces each: their
+  // workgroups follow all whole items in the same launch (so they fill the
+  // compute units as the last whole items finish), then a merge kernel.
+  const int split = sp.s, n_split = sp.n;
+  const int last = n - 1;
+  const int items_last = w.prefix[n] - w.prefix[last];
+  AttnWork wp = w;
+  wp.prefix[n] -= n_split;   // whole items: all but those
+  if (n_split == items_last) wp.n_req = last;
+  SplitState* st = split_state();   // exists: choose_split checked
+  std::lock_guard<std::mutex> lock(st->mu);
+  if (st->used) {
+    const hipError_t e = hipStreamWaitEvent(s, st->done, 0);   // the previous call's merge has read the pieces
+    if (e != hipSuccess) return e;
+  }
+  wp.split_s = split;
+  wp.split_req = last;
+  wp.split_first = items_last - n_split;
+  wp.split_base = grid_of(wp);
+  wp.split_n = n_split * split;
+  wp.part = st->part;
+  launch(wp, wp.split_base + wp.split_n);
+  attn_merge_kernel<<<n_split * 256 / 4, 256, 0, s>>>((bf16*)p.o, p.o_stride, st->part, wp.split_n, wp);
+  const hipError_t e = hipEventRecord(st->done, s);
+  if (e != hipSuccess) return e;
+  st->used = true;
 #undef DIT_ATTN_ARGS
   return hipGetLastError();
 }

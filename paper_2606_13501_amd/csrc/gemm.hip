@@ -570,18 +570,6 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(
   }
 }
 
-// Compute units of the current device (cached per device).
-int cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
-  }
-  return cached[dev];
-}
 
 std::atomic<int> g_tile_n{0};   // forced output tile width (0: chosen per shape)
 
@@ -635,6 +623,19 @@ hipError_t launch_f32(const LinearArgs& p, hipStream_t s) {
 }
 
 }  // namespace
+
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 void set_gemm_tile_n(int bn) { g_tile_n.store(bn, std::memory_order_relaxed); }
 

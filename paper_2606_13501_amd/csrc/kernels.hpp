@@ -28,6 +28,8 @@ struct LinearArgs {
   int64_t plane_stride = 0;
 };
 hipError_t launch_linear(const LinearArgs& p, hipStream_t s);
+// Compute units of the current device (cached per device).
+int cu_count();
 // Forces the bf16 GEMM's output tile width (192 or 256; 0: chosen per shape).
 void set_gemm_tile_n(int bn);
 
@@ -45,6 +47,8 @@ struct AttnArgs {
   float q_eps = 0.f;
 };
 hipError_t launch_attention(const AttnArgs& p, hipStream_t s);
+// bf16 self-attention's split of its last round (0 per shape, 1 never, 2 or 4 forced).
+void set_attention_split(int mode);
 
 // out = LN(x) * mul + add, mul/add per request (modulate: mul = 1 + scale) or
 // shared (affine: gamma, beta).

@@ -134,6 +134,15 @@ def test_gemm_tile_width_hook():
         assert L.dit_debug_gemm_tile_n(good) == B.DIT_OK
 
 
+def test_attention_split_hook():
+    L = _lib()
+    for bad in (3, 8, -1, 5):
+        assert L.dit_debug_attention_split(bad) == B.DIT_ERR_INVALID_ARG
+        assert b"split mode" in L.dit_last_error()
+    for good in (1, 2, 4, 0):   # ends on 0: the per-shape choice
+        assert L.dit_debug_attention_split(good) == B.DIT_OK
+
+
 def test_norm_kernels_reject_bad_arguments():
     L = _lib()
     S = ctypes.c_void_p(0)

@@ -238,6 +238,57 @@ def test_attention_varlen(dtype, H, d, lq, lk):
     check(host(out), ref, dtype, "attention")
 
 
+class forced_attention_split:
+    """Force the bf16 attention's split into key pieces (2 or 4) inside a
+    with-block; the choice per shape again afterwards."""
+
+    def __init__(self, B, mode):
+        self.B, self.mode = B, mode
+
+    def __enter__(self):
+        self.B.debug_attention_split(self.mode)
+
+    def __exit__(self, *exc):
+        self.B.debug_attention_split(0)
+
+
+SPLIT_CASES = [
+    # heads, query lengths, key lengths (None = self-attention)
+    (2, [3000], None),                 # all 24 items split; keys ragged (47 tiles of 64, the last of 56)
+    (2, [2600, 2100], None),           # the second request's 18 items split, the first's run whole
+    (1, [300, 200], [4000, 2100]),     # cross-shaped ranges over 1024 keys, ragged in queries and keys
+]
+
+
+@pytest.mark.parametrize("pieces", [2, 4])
+@pytest.mark.parametrize("H,lq,lk", SPLIT_CASES)
+def test_attention_split_into_key_pieces(H, lq, lk, pieces):
+    """Work items computed as 2 or 4 key pieces and merged equal the oracle;
+    a second split call right after (another shape) reuses the pieces' array
+    and is correct too."""
+    B = require_gpu()
+    d = 128
+    cu_q = _cu(lq)
+    cu_k = cu_q if lk is None else _cu(lk)
+    Tq, Tk, W = int(cu_q[-1]), int(cu_k[-1]), H * d
+    qb = synth.draw((Tq, W), (34, H, Tq, Tk), "bf16")
+    kvb = synth.draw((Tk, 2 * W), (35, H, Tq, Tk), "bf16")
+    ref = O.attention_varlen(O.decode(qb), O.decode(kvb)[:, :W], O.decode(kvb)[:, W:], cu_q, cu_k, H, d)
+    # the second call: one request of 2500 rows, 1 head, self-attention
+    qb2 = synth.draw((2500, 3 * d), (36, 1, 2500), "bf16")
+    ref2 = O.attention_varlen(O.decode(qb2)[:, :d], O.decode(qb2)[:, d:2 * d], O.decode(qb2)[:, 2 * d:],
+                              _cu([2500]), _cu([2500]), 1, d)
+    log(f"case attention split H={H} lq={lq} lk={lk} pieces={pieces}")
+    qt, kvt, q2 = dev(qb), dev(kvb), dev(qb2)
+    out, out2 = empty((Tq, W), "bf16"), empty((2500, d), "bf16")
+    with forced_attention_split(B, pieces):
+        B.attention_varlen(qt, kvt[:, :W], kvt[:, W:], out, cu_q, cu_k, H, d)
+        B.attention_varlen(q2[:, :d], q2[:, d:2 * d], q2[:, 2 * d:], out2, _cu([2500]), _cu([2500]), 1, d)
+        torch.cuda.synchronize()
+    check(host(out), ref, "bf16", f"attention split into {pieces}")
+    check(host(out2), ref2, "bf16", f"attention split into {pieces}, second call")
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
 def test_attention_request_without_keys(dtype, d):
     """A request with queries but no keys gets rows of zeros; the packed
