@@ -323,20 +323,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     mma(f0);
     if (!first) io4(P, 4, s + 1, s + 3, stP, ldP);
     pattern();
+    __builtin_amdgcn_sched_barrier(0);   // the quarter's reads stay in the quarter
     read(f0, s, 2);
     mma(f1);
     if (!first) io4(P, 8, s + 1, s + 3, stP, ldP);
     pattern();
+    __builtin_amdgcn_sched_barrier(0);   // the quarter's reads stay in the quarter
     read(f1, s, 3);
     mma(f0);
     if (!first) io4(P, 12, s + 1, s + 3, stP, ldP);
     pattern();
+    __builtin_amdgcn_sched_barrier(0);   // the quarter's reads stay in the quarter
     __syncthreads();
     if (dma >= 0) dma_step(dma);
     read(f0, s + 1, 0);   // after the last step: a harmless read of the idle slot
     mma(f1);
     io4(Q, 0, s + 2, s + 4, stQ, ldQ);
     pattern();
+    __builtin_amdgcn_sched_barrier(0);   // the quarter's reads stay in the quarter
   };
   // first tile: slots 0 and 1 get steps 0 and 1 through the register stages
   // (with fewer K steps, steps past the end reload the last one; they fill
