@@ -227,36 +227,46 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[i], f.a[j], acc[i][j], 0, 0, 0);
   };
   const int KT = K / BK;
-  // Per K quarter: 16 MFMAs, 8 fragment reads, and (when a register stage
-  // is being cycled) 4 LDS stores + 4 global loads, spread evenly: per 4
-  // MFMAs 2 reads, 1 store and 1 load.  An even stream of global loads keeps
-  // the memory pipeline busy without bursts that would stall MFMA issue.
-  // (With 3 W blocks per wave: 12 MFMAs, 7 reads, up to 4 stores and 4 loads
-  // per quarter, as MFMA, read, MFMA, store, MFMA, read (not in the last
-  // group), load.)
+  // Per K quarter: 16 MFMAs, the 8 fragment reads of the next quarter, and
+  // (when a register stage is being cycled) 4 LDS stores + 4 global loads.
+  // The reads go first, one per MFMA over the first half, so each has most
+  // of a quarter to land; the stores and loads are spread over the second
+  // half.  (Measured at 720p against reads, stores and loads interleaved
+  // evenly: QKV 8.85 against 9.16 ms; reads two per MFMA or loads before
+  // stores were no better.)  With 3 W blocks per wave: 12 MFMAs, 7 reads, up
+  // to 4 stores and 4 loads per quarter, in the same order.  Each quarter is
+  // closed by a scheduling fence (below), so the compiler cannot sink the
+  // next quarter's reads next to the MFMAs that consume them.
   auto pattern = [] {
+    if constexpr (NI == 4) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if constexpr (NI == 4) {
+      for (int i = 0; i < 8; ++i) {   // the next quarter's 8 reads, one per MFMA of the first half
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {   // stores and loads over the second half
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      } else {
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 7; ++i) {   // the next quarter's 7 reads, one per MFMA
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {   // stores and loads over the remaining MFMAs
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       }
     }
   };
+
+
   // items u0 .. u0 + 3 of a register stage (items 0-7: A pieces, 8-15: W
   // pieces): store each into the LDS slot of step st_step, then reload it
   // with step ld_step (each part only when asked for)
