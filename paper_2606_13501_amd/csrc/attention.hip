@@ -103,8 +103,10 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_
 // would otherwise place the scores in accumulation registers and copy them to
 // vector registers for the softmax.  It does not see these as MFMAs, so the
 // distance from the last MFMA of a score block to its first vector read is
-// kept by hand: score_guard (at least 19 wait states) takes the block as an
-// in-out operand, so no read of it can be scheduled before the guard.
+// kept by hand: the last MFMA pair of a tile and the wait states after it
+// (13; the compiler puts 12 between this MFMA and a vector read of its
+// result) are one asm statement, so nothing that reads the scores, not even
+// a register copy the allocator adds, can come between them.
 __device__ __forceinline__ void mfma_s_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
   // d as an in-out operand (its old value unused) keeps the scores in the
   // same registers from tile to tile, without copies
@@ -118,7 +120,14 @@ __device__ __forceinline__ void mfma_s_bias(f32x16& d, const bf16x8& a, const bf
 __device__ __forceinline__ void mfma_s_acc(f32x16& d, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "v"(b));
 }
-__device__ __forceinline__ void score_guard(f32x16& d) { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4" : "+v"(d)); }
+// the last MFMA of both score blocks, then the wait states
+__device__ __forceinline__ void mfma_s_last(f32x16& d0, f32x16& d1, const bf16x8& a0, const bf16x8& a1,
+                                            const bf16x8& b) {
+  asm volatile(
+      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, %0\n\tv_mfma_f32_32x32x16_bf16 %1, %3, %4, %1\n\ts_nop 7\n\ts_nop 4"
+      : "+v"(d0), "+v"(d1)
+      : "v"(a0), "v"(a1), "v"(b));
+}
 
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
@@ -302,7 +311,9 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
         ka[kc + 1] = *reinterpret_cast<const bf16x8*>(smem + (so ^ ((kc + 1) << 5)));
         kb[kc + 1] = *reinterpret_cast<const bf16x8*>(smem + (so ^ ((kc + 1) << 5)) + 32 * 256);
       }
-      if (kc > 0) {
+      if (kc == 7) {
+        mfma_s_last(sq[0], sq[1], ka[7], kb[7], qf[7]);
+      } else if (kc > 0) {
         mfma_s_acc(sq[0], ka[kc], qf[kc]);
         mfma_s_acc(sq[1], kb[kc], qf[kc]);
       } else if (decltype(first)::value) {
@@ -313,8 +324,6 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
         mfma_s_bias(sq[1], kb[0], qf[0], nref);
       }
     }
-    score_guard(sq[0]);
-    score_guard(sq[1]);
   };
   // P(t) from S(t).  FIRST: S(t) came from zero (the reference is set, in the
   // first pass, and subtracted here); LAST: keys past the request end -> -inf
