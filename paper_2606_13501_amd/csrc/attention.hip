@@ -78,23 +78,18 @@ struct AttnWork {
   float* part;
 };
 
-// Raw buffer descriptor over `bytes` bytes from `base`: loads past the end
-// return zeros.
-__device__ __forceinline__ u32x4 make_desc(const void* base, int64_t bytes) {
-  const uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)(bytes < 0 ? 0 : bytes);
-  const uint64_t p = (uint64_t)base;
-  return u32x4{(uint32_t)p, (uint32_t)(p >> 32) & 0xFFFFu, n, 0x00020000u};
-}
-
 // 16 bytes per lane from global memory straight into LDS: lane i writes LDS
-// bytes lds + 16 i .. +15.  Inline assembly, so the compiler does not make
-// every later LDS read wait for it; completion is tracked by hand
-// (wait_vmcnt) and the workgroup barrier publishes the data.
+// bytes lds + OFF + 16 i .. +15 (one scalar add into m0 per load).  Inline
+// assembly, so the compiler does not make every later LDS read wait for it;
+// completion is tracked by hand (wait_vmcnt) and the workgroup barrier
+// publishes the data.  Raw buffer descriptors (stride 0): loads past the
+// record count return zeros.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
+template <uint32_t OFF>
 __device__ __forceinline__ void load_lds16(const u32x4& desc, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(lds), "v"(voff), "s"(desc) : "m0");
+  asm volatile("s_add_u32 m0, %0, %3\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds), "v"(voff), "s"(desc), "n"(OFF) : "m0", "scc");
 }
 #pragma clang diagnostic pop
 template <int N> __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N)); }
@@ -252,16 +247,45 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
     v_voff[u] = (uint32_t)(row * (int)vs * 2 + ((pc ^ (4 * (row & 3))) << 4));
   }
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_char*)smem;
-  // rows past the request's last key read as zero (descriptor bound)
+  // Rows past the request's last key read as zero (descriptor bound).  The
+  // tiles are issued in order, so the next tile's base addresses and its
+  // rows left advance by one tile per issue: a few scalar instructions
+  // instead of 64-bit products and clamps per tile, which all eight waves
+  // would otherwise run on the one scalar unit of the compute unit right
+  // after each barrier.  The record count is capped at the 32-bit range.
+  const uint32_t k_row_b = (uint32_t)ks * 2u, v_row_b = (uint32_t)vs * 2u;
+  const int cap_rows = (int)min((uint32_t)INT_MAX, 0xFFFFFFFFu / max(max(k_row_b, v_row_b), 1u));
+  uint64_t k_next = 0, v_next = 0;
+  int rows_left = 0;
+  auto rewind = [&]() __attribute__((always_inline)) {
+    k_next = (uint64_t)(uintptr_t)k_head;
+    v_next = (uint64_t)(uintptr_t)v_head;
+    rows_left = n_k;
+  };
   auto issue = [&](int t) __attribute__((always_inline)) {
-    const int kb = t * BKV;
-    const u32x4 kd = make_desc(k_head + (int64_t)kb * ks, (int64_t)(n_k - kb) * ks * 2);
-    const u32x4 vd = make_desc(v_head + (int64_t)kb * vs, (int64_t)(n_k - kb) * vs * 2);
+    const uint32_t rows = (uint32_t)min(max(rows_left, 0), cap_rows);
+    const u32x4 kd = u32x4{(uint32_t)k_next, (uint32_t)(k_next >> 32) & 0xFFFFu, rows * k_row_b, 0x00020000u};
+    const u32x4 vd = u32x4{(uint32_t)v_next, (uint32_t)(v_next >> 32) & 0xFFFFu, rows * v_row_b, 0x00020000u};
+    k_next += (uint64_t)(BKV * k_row_b);
+    v_next += (uint64_t)(BKV * v_row_b);
+    rows_left -= BKV;
     const uint32_t st = lds_base + (uint32_t)((t % RING) * kSlotBytes) + kPieces * wave * 1024;
 #pragma unroll
     for (int u = 0; u < kPieces; ++u) {
-      load_lds16(kd, k_voff[u], st + u * 1024);
-      load_lds16(vd, v_voff[u], st + kTileBytes + u * 1024);
+      static_assert(kPieces <= 4, "LDS offsets below");
+      if (u == 0) {
+        load_lds16<0>(kd, k_voff[u], st);
+        load_lds16<kTileBytes>(vd, v_voff[u], st);
+      } else if (u == 1) {
+        load_lds16<1024>(kd, k_voff[u], st);
+        load_lds16<kTileBytes + 1024>(vd, v_voff[u], st);
+      } else if (u == 2) {
+        load_lds16<2048>(kd, k_voff[u], st);
+        load_lds16<kTileBytes + 2048>(vd, v_voff[u], st);
+      } else {
+        load_lds16<3072>(kd, k_voff[u], st);
+        load_lds16<kTileBytes + 3072>(vd, v_voff[u], st);
+      }
     }
   };
 
@@ -385,15 +409,24 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
   // and tile t + 3 goes into the slot of tile t - 1, which every wave has
   // finished.  Ring of 2: tile t + 1 is the only one in flight, and tile
   // t + 2 goes into the slot of tile t, which every wave has just finished.
-  auto step = [&](int t, auto first, auto last, auto track) __attribute__((always_inline)) {
+  // STEADY: a middle tile with at least kAhead tiles after it (the deeper
+  // wait and the issue are unconditional: no per-tile scalar tests)
+  auto step = [&](int t, auto first, auto last, auto track, auto steady) __attribute__((always_inline)) {
     S(t, first);
     softmax(t, first, last, track);
     PV(t);
     if (!decltype(last)::value) {
-      if (RING == 4 && t + 2 < n_tiles) wait_vmcnt<kLoadsPerTile>();
-      else wait_vmcnt<0>();
-      __syncthreads();
-      if (t + kAhead < n_tiles) issue(t + kAhead);
+      if (decltype(steady)::value) {
+        if (RING == 4) wait_vmcnt<kLoadsPerTile>();
+        else wait_vmcnt<0>();
+        __syncthreads();
+        issue(t + kAhead);
+      } else {
+        if (RING == 4 && t + 2 < n_tiles) wait_vmcnt<kLoadsPerTile>();
+        else wait_vmcnt<0>();
+        __syncthreads();
+        if (t + kAhead < n_tiles) issue(t + kAhead);
+      }
     }
   };
   using kOn = std::true_type;
@@ -403,6 +436,7 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
     for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
     l_run[0] = l_run[1] = l_run[2] = l_run[3] = 0.f;
     x_max = -INFINITY;
+    rewind();
     const int n_pre = min(kAhead, n_tiles);
     for (int t = 0; t < n_pre; ++t) issue(t);
     // tile 0 in LDS
@@ -411,17 +445,19 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
     else wait_vmcnt<0>();
     __syncthreads();
     if (n_tiles == 1) {
-      step(0, kOn{}, kOn{}, track);
+      step(0, kOn{}, kOn{}, track, kOff{});
     } else {
-      step(0, kOn{}, kOff{}, track);
+      step(0, kOn{}, kOff{}, track, kOff{});
       // no compiler-tracked load may still be pending when the loop starts:
       // its tracking would otherwise put a vmcnt wait (which also waits for
       // the tile loads in flight) at the top of every iteration.  (The short
       // shape's items are a few tiles long: there this wait would cost a
       // tile's load latency per item.)
       if constexpr (RING == 4) __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), once per work item
-      for (int t = 1; t + 1 < n_tiles; ++t) step(t, kOff{}, kOff{}, track);
-      step(n_tiles - 1, kOff{}, kOn{}, track);
+      int t = 1;
+      for (; t + kAhead < n_tiles; ++t) step(t, kOff{}, kOff{}, track, kOn{});
+      for (; t + 1 < n_tiles; ++t) step(t, kOff{}, kOff{}, track, kOff{});
+      step(n_tiles - 1, kOff{}, kOn{}, track, kOff{});
     }
   };
 
