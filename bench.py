@@ -34,6 +34,81 @@ PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "attn_fwd_bf16.video_720p.traff
 ATTN_SOURCE = os.path.join(ROOT, "paper_2606_13501_amd", "csrc", "attention.hip")
 
 
+
+class GpuSensors:
+    """Power and shader clock of the GPU while the timed steps run.
+
+    A background thread reads sysfs every `period` seconds: the board power
+    (`hwmon*/power1_input`, microwatts) and the current shader clock (the line
+    of `pp_dpm_sclk` marked with `*`).  These are file reads only; no external
+    tool is started.  On a box with several GPUs the first card that exposes
+    the files is read.  Missing files give None."""
+
+    def __init__(self, period=0.02, root="/sys/class/drm"):
+        import glob
+        cards = sorted(glob.glob(os.path.join(root, "card*", "device", "pp_dpm_sclk")))
+        self.sclk = cards[0] if cards else None
+        dev = os.path.dirname(self.sclk) if self.sclk else ""
+        power = sorted(glob.glob(os.path.join(dev, "hwmon", "hwmon*", "power1_input"))) if dev else []
+        self.power = power[0] if power else None
+        self.cap = os.path.join(os.path.dirname(self.power), "power1_cap") if self.power else None
+        self.period = period
+        self.watts, self.mhz = [], []
+        self._stop = None
+        self._thread = None
+
+    @staticmethod
+    def _read(path):
+        try:
+            with open(path) as f:
+                return f.read()
+        except OSError:
+            return None
+
+    def _sample(self):
+        if self.power:
+            v = self._read(self.power)
+            if v and v.strip().isdigit():
+                self.watts.append(int(v) / 1e6)
+        if self.sclk:
+            v = self._read(self.sclk)
+            for line in (v or "").splitlines():
+                if line.rstrip().endswith("*"):
+                    num = "".join(ch for ch in line.split(":", 1)[-1] if ch.isdigit())
+                    if num:
+                        self.mhz.append(int(num))
+
+    def __enter__(self):
+        import threading
+        if self.power or self.sclk:
+            self._stop = threading.Event()
+
+            def loop():
+                while not self._stop.is_set():
+                    self._sample()
+                    self._stop.wait(self.period)
+
+            self._thread = threading.Thread(target=loop, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self._thread is not None:
+            self._stop.set()
+            self._thread.join()
+        return False
+
+    def summary(self):
+        cap = self._read(self.cap) if self.cap else None
+        w, m = self.watts, sorted(self.mhz)
+        return {
+            "gpu_power_w_mean": round(sum(w) / len(w), 1) if w else None,
+            "gpu_power_w_max": round(max(w), 1) if w else None,
+            "gpu_power_cap_w": round(int(cap) / 1e6, 1) if cap and cap.strip().isdigit() else None,
+            "gpu_sclk_mhz_median": m[len(m) // 2] if m else None,
+            "gpu_sensor_samples": len(w),
+        }
+
 def block_flops(wl):
     """Algorithmic flops of one block (2 per multiply-add; attention 4 n^2 H d
     non-causal for self, 4 n L H d for cross)."""
@@ -210,11 +285,12 @@ def run_step(args):
         print(f"[bench] warmup step {i} done", file=sys.stderr, flush=True)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        one(args.warmup + i)
-    stop.record(stream)
-    torch.cuda.synchronize()
+    with GpuSensors() as sensors:
+        start.record(stream)
+        for i in range(args.steps):
+            one(args.warmup + i)
+        stop.record(stream)
+        torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     if not torch.isfinite(lat[(args.warmup + args.steps) % 2]).all():
         raise RuntimeError("non-finite latent after the timed steps")
@@ -240,6 +316,7 @@ def run_step(args):
             "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
             "ms_text_kv_once_per_request": round(k0.elapsed_time(k1), 3),
             "ms_per_block": round(ms / mw.n_blocks, 3),
+            **sensors.summary(),
         },
         "roofline": {
             "kernel": "whole step (per-kernel durations: rocprofv3 kernel statistics of this command)",
@@ -675,13 +752,14 @@ def main():
     sevs = [new_ev() for _ in range(args.steps)]
     start, stop = new_ev()
     torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        sevs[i][0].record(stream)
-        step(evs[i])
-        sevs[i][1].record(stream)
-    stop.record(stream)
-    torch.cuda.synchronize()
+    with GpuSensors() as sensors:
+        start.record(stream)
+        for i in range(args.steps):
+            sevs[i][0].record(stream)
+            step(evs[i])
+            sevs[i][1].record(stream)
+        stop.record(stream)
+        torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     attn_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
     step_ms = sorted(a.elapsed_time(b) for a, b in sevs)
@@ -740,6 +818,7 @@ def main():
             "ms_step_median": round(step_ms[len(step_ms) // 2], 3), "ms_step_min": round(step_ms[0], 3),
             "ms_step_cold_median": round(cold[len(cold) // 2], 3) if cold else None,
             "ms_step_cold_min": round(cold[0], 3) if cold else None,
+            **sensors.summary(),
         },
         "roofline": {
             "kernel": "attn_fwd_bf16 (self-attention)" if wl.dtype == "bf16" else "attn_fwd_f32 (self-attention)",
