@@ -554,6 +554,31 @@ def profile_kernel(args, wl):
     T, D, H, hd = wl.n_rows, wl.hidden, wl.n_heads, wl.head_dim
     g = torch.Generator(device="cuda")
     g.manual_seed(13501)
+    if args.profile_kernel == "gated_residual":
+        # the unfused gated residual (the block fuses it into the GEMM
+        # epilogues): y = x + gate * (z + bias), timed with HIP events
+        x = torch.randn((T, D), generator=g, device="cuda").to(torch.bfloat16)
+        z = torch.randn((T, D), generator=g, device="cuda").to(torch.bfloat16)
+        bias = (torch.randn((D,), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+        gate = torch.randn((wl.n_req, D), generator=g, device="cuda")
+        y = torch.empty_like(x)
+        cu = wl.cu_seqlens()
+        for _ in range(2):
+            B.gated_residual(x, z, bias, gate, D, cu, y)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(args.steps):
+            B.gated_residual(x, z, bias, gate, D, cu, y)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / args.steps
+        alg = 3 * 2 * T * D   # x and z read, y written, once
+        print(json.dumps({"profile": "gated_residual", "workload": wl.name, "launches": args.steps,
+                          "ms_per_launch": round(ms, 4), "algorithmic_bytes": alg,
+                          "achieved_gbs": round(alg / (ms * 1e-3) / 1e9, 1),
+                          "frac_of_hbm_peak": round(alg / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}), flush=True)
+        return
     qkv = torch.randn((3, T, D), generator=g, device="cuda").to(torch.bfloat16)   # q, k, v planes
     o = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
     cu = wl.cu_seqlens()
@@ -635,10 +660,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="video_720p")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-kernel", choices=["attention", "copy"], default=None,
+    ap.add_argument("--profile-kernel", choices=["attention", "copy", "gated_residual"], default=None,
                     help="run only one kernel (for rocprofv3 counter passes) and exit: the block's "
-                         "self-attention at the workload's shape, or a plain 1 GiB device copy used to "
-                         "calibrate the HBM byte counters")
+                         "self-attention at the workload's shape, a plain 1 GiB device copy used to "
+                         "calibrate the HBM byte counters, or the unfused gated residual at the "
+                         "workload's shape (timed; prints GB/s)")
     ap.add_argument("--step", default=None, metavar="STEP_WORKLOAD",
                     help="time one whole denoising step (dit_denoise_step) at this step workload, e.g. "
                          "step_video_720p, instead of the block; prints its own JSON line")
