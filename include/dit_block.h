@@ -194,7 +194,9 @@ dit_status dit_timestep_modulation_noalloc(const dit_block_config *cfg, const di
  * value is used as given (inf or NaN: DIT_ERR_INVALID_ARG).  o must not
  * overlap q, k or v: the byte range from o's first to its last row must not
  * meet that of q, k or v (checked, DIT_ERR_INVALID_ARG); q, k and v may share
- * one buffer.  bf16 needs head_dim 128; fp32 takes 64 or 128.  A request with
+ * one buffer.  bf16 needs head_dim 128, and k_row_stride and v_row_stride of
+ * at most 2^24 elements (the kernel forms a key tile's offsets in 32 bits;
+ * larger: DIT_ERR_INVALID_ARG); fp32 takes 64 or 128.  A request with
  * queries but no keys gets rows of zeros. */
 dit_status dit_attention_varlen(const void *q, const void *k, const void *v, void *o,
                                 int64_t q_row_stride, int64_t k_row_stride,

@@ -808,6 +808,10 @@ dit_status dit_attention_varlen(const void* q, const void* k, const void* v, voi
     if (strides[i] < width || strides[i] % vec)
       return fail(DIT_ERR_INVALID_ARG, "row stride %lld: must be >= n_heads*head_dim = %lld and a multiple of %lld",
                   (long long)strides[i], (long long)width, (long long)vec);
+  // the bf16 kernel forms a key tile's offsets (64 rows of k or v) in 32 bits
+  if (dtype == DIT_BF16 && (k_row_stride > (int64_t)1 << 24 || v_row_stride > (int64_t)1 << 24))
+    return fail(DIT_ERR_INVALID_ARG, "k/v row stride %lld / %lld: at most %lld elements for bf16",
+                (long long)k_row_stride, (long long)v_row_stride, (long long)1 << 24);
   // o is written while q, k and v are still being read: its byte range must
   // not meet theirs (ranges from the first to the last byte a row touches)
   const int64_t es = (int64_t)elem_size(dtype);

@@ -81,6 +81,11 @@ def test_attention_rejects_bad_arguments():
     assert call(P, pcu, pcu, 1, 1, 64, 0.1, B.DIT_BF16) == B.DIT_ERR_UNSUPPORTED
     assert call(P, pcu, pcu, 1, 1, 96, 0.1, B.DIT_F32) == B.DIT_ERR_UNSUPPORTED
     assert call(P, pcu, pcu, 1, 2, 128, 0.1, B.DIT_BF16) == B.DIT_ERR_INVALID_ARG   # stride < H*d
+    # k / v row strides past 2^24 elements (the bf16 kernel's 32-bit tile offsets)
+    big = lambda ks, vs: L.dit_attention_varlen(P, PK, PV, PO, 128, ks, vs, 128, pcu, pcu, 1, 1, 128, 0.1,
+                                                B.DIT_BF16, S)
+    assert big((1 << 24) + 8, 128) == B.DIT_ERR_INVALID_ARG and b"at most" in L.dit_last_error()
+    assert big(128, (1 << 24) + 8) == B.DIT_ERR_INVALID_ARG and b"at most" in L.dit_last_error()
     assert call(P, pcu, pcu, 1, 1, 128, float("inf"), B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
     assert call(P, pcu, pcu, 1, 1, 128, float("nan"), B.DIT_BF16) == B.DIT_ERR_INVALID_ARG
     assert b"softmax_scale" in L.dit_last_error()
