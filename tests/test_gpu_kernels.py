@@ -214,6 +214,11 @@ ATTN_CASES = [
     ("bf16", 3, 128, [1, 255, 256, 700, 64], None),
     ("bf16", 2, 128, [100, 0, 513], [77, 40, 512]),
     ("bf16", 1, 128, [2048], None),
+    # the 8-wave shape (a key range over 1024) with requests of 1 to 5 key
+    # tiles beside a long one: the loop's first, steady, tail and last steps
+    ("bf16", 2, 128, [1100, 1, 64, 65, 190, 256, 257, 320], None),
+    # the 4-wave shape with 2, 3, 4 and 16 key tiles
+    ("bf16", 2, 128, [65, 129, 193, 5], [65, 129, 193, 1000]),
     ("f32", 6, 64, [64], None),
     ("f32", 6, 64, [64], [77]),
     ("f32", 2, 128, [5, 30], [7, 1]),
