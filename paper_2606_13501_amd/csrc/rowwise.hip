@@ -381,6 +381,75 @@ __global__ __launch_bounds__(256) void gemv_kernel(const T* __restrict__ W, cons
   }
 }
 
+// The same product for rows of at most 64 NVL vectors: a lane loads all of
+// its NVL weight vectors of the row first, so they are in flight together
+// (the weights stream from memory once, and a wave with one load in flight
+// at a time is latency-bound), then accumulates each request over them in
+// the order of gemv_kernel (the results are the same bits).
+template <typename T, bool SILU_OUT, int NVL>
+__global__ __launch_bounds__(256) void gemv_row_kernel(const T* __restrict__ W, const T* __restrict__ b,
+                                                       const float* __restrict__ x, float* __restrict__ y,
+                                                       int n_out, int n_in, int n_req) {
+  typedef typename Vec16<T>::type V;
+  constexpr int VN = Vec16<T>::n;
+  typedef float fxv __attribute__((ext_vector_type(VN)));
+  const int lane = threadIdx.x & 63;
+  const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (o >= n_out) return;
+  const T* wr = W + (int64_t)o * n_in;
+  const int nv = n_in / VN;
+  const float bo = b ? to_f<T>(b[o]) : 0.f;
+  // FULL: every lane has all NVL vectors (no per-lane tests, so the loads
+  // are not split by branches)
+  auto run = [&](auto full) __attribute__((always_inline)) {
+    V wv[NVL];
+#pragma unroll
+    for (int u = 0; u < NVL; ++u) {
+      const int c = lane + 64 * u;
+      if (decltype(full)::value || c < nv) wv[u] = *reinterpret_cast<const V*>(wr + c * VN);
+    }
+    for (int r = 0; r < n_req; ++r) {
+      const float* xr = x + (int64_t)r * n_in;
+      fxv xv[NVL];   // the request's inputs under the lane's vectors, loaded together
+#pragma unroll
+      for (int u = 0; u < NVL; ++u) {
+        const int c = lane + 64 * u;
+        if (decltype(full)::value || c < nv) xv[u] = *reinterpret_cast<const fxv*>(xr + c * VN);
+      }
+      float acc = 0.f;
+#pragma unroll
+      for (int u = 0; u < NVL; ++u) {
+        const int c = lane + 64 * u;
+        if (decltype(full)::value || c < nv) {
+#pragma unroll
+          for (int e = 0; e < VN; ++e) acc = fmaf(to_f<T>(wv[u][e]), xv[u][e], acc);
+        }
+      }
+      float sum = wave_sum(acc);
+      if (lane == 0) {
+        sum += bo;
+        y[(int64_t)r * n_out + o] = SILU_OUT ? silu(sum) : sum;
+      }
+    }
+  };
+  if (nv == 64 * NVL) run(std::true_type{});
+  else run(std::false_type{});
+}
+
+template <typename T, bool SILU_OUT>
+void launch_gemv(const T* W, const T* b, const float* x, float* y, int n_out, int n_in, int n_req, hipStream_t s) {
+  const unsigned grid = (unsigned)((n_out + 3) / 4);
+  switch ((n_in / Vec16<T>::n + 63) / 64) {
+#define DIT_GEMV_ROW(NVL) \
+  case NVL: gemv_row_kernel<T, SILU_OUT, NVL><<<grid, 256, 0, s>>>(W, b, x, y, n_out, n_in, n_req); return;
+    DIT_GEMV_ROW(1) DIT_GEMV_ROW(2) DIT_GEMV_ROW(3) DIT_GEMV_ROW(4) DIT_GEMV_ROW(5) DIT_GEMV_ROW(6)
+    DIT_GEMV_ROW(7) DIT_GEMV_ROW(8) DIT_GEMV_ROW(9) DIT_GEMV_ROW(10) DIT_GEMV_ROW(11) DIT_GEMV_ROW(12)
+    DIT_GEMV_ROW(13) DIT_GEMV_ROW(14) DIT_GEMV_ROW(15) DIT_GEMV_ROW(16)
+#undef DIT_GEMV_ROW
+    default: gemv_kernel<T, SILU_OUT><<<grid, 256, 0, s>>>(W, b, x, y, n_out, n_in, n_req);
+  }
+}
+
 template <typename T, int NVL>
 hipError_t gres_nvl(const GatedResArgs& p, hipStream_t s) {
   gated_residual_kernel<T, NVL><<<(unsigned)((p.n_rows + 3) / 4), 256, 0, s>>>(
@@ -446,15 +515,12 @@ hipError_t cond_typed(const CondArgs& p, hipStream_t s) {
   if (p.w_t1) {
     const int half = p.freq_dim / 2;
     timestep_embed_kernel<<<(p.n_req * half + 255) / 256, 256, 0, s>>>(p.t, p.e, p.n_req, p.freq_dim);
-    gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t1, (const T*)p.b_t1, p.e, p.a1,
-                                                           p.hidden, p.freq_dim, p.n_req);
-    gemv_kernel<T, true><<<(p.hidden + 3) / 4, 256, 0, s>>>((const T*)p.w_t2, (const T*)p.b_t2, p.a1, p.c,
-                                                           p.hidden, p.hidden, p.n_req);
+    launch_gemv<T, true>((const T*)p.w_t1, (const T*)p.b_t1, p.e, p.a1, p.hidden, p.freq_dim, p.n_req, s);
+    launch_gemv<T, true>((const T*)p.w_t2, (const T*)p.b_t2, p.a1, p.c, p.hidden, p.hidden, p.n_req, s);
   }
   if (p.w_ada) {
     const int n_out = p.n_mod * p.hidden;
-    gemv_kernel<T, false><<<(n_out + 3) / 4, 256, 0, s>>>((const T*)p.w_ada, (const T*)p.b_ada, p.c, p.mod,
-                                                         n_out, p.hidden, p.n_req);
+    launch_gemv<T, false>((const T*)p.w_ada, (const T*)p.b_ada, p.c, p.mod, n_out, p.hidden, p.n_req, s);
   }
   return hipGetLastError();
 }
