@@ -23,6 +23,16 @@ SMALL_PACKED = Workload(
     txt_len=64, linear_std=0.02 * (5120 / 512) ** 0.5, description="small packed bf16 batch for parity")
 
 
+# The video blocks' own shape and weight scale (D = 5120, 40 x 128 heads, MLP
+# 13824, rotary sections 44/42/42, Linear weights N(0, 0.02^2) as in the
+# 480p and 720p configurations) on two short requests (300 and 180 tokens,
+# 512 text tokens each), so every row of a config-scale block is compared.
+VIDEO_SMALL = Workload(
+    name="video_small_d5120", wid=51, dtype="bf16", hidden=5120, n_heads=40, head_dim=128, mlp_hidden=13824,
+    freq_dim=5120, rope_sections=(44, 42, 42), grids=((1, 15, 20), (3, 6, 10)), rows=(300, 180), txt_len=512,
+    description="two short video requests at the video blocks' width and weight scale")
+
+
 def _oracle_block(db: DeviceBlock, x=None):
     wl = db.wl
     w = db.oracle_weights()
@@ -32,9 +42,9 @@ def _oracle_block(db: DeviceBlock, x=None):
     return O.block_forward(cfg, vl, xx, w["t"], w["txt"], w)
 
 
-@pytest.mark.parametrize("name", ["tiny_image_fp32", "image_1024", "small_packed_bf16"])
+@pytest.mark.parametrize("name", ["tiny_image_fp32", "image_1024", "small_packed_bf16", "video_small_d5120"])
 def test_block_parity(name):
-    wl = SMALL_PACKED if name == "small_packed_bf16" else synth.get_workload(name)
+    wl = {"small_packed_bf16": SMALL_PACKED, "video_small_d5120": VIDEO_SMALL}.get(name) or synth.get_workload(name)
     log(f"case block parity {name}")
     db = DeviceBlock(wl)
     y = db.forward()
