@@ -252,6 +252,28 @@ dit_status dit_debug_gemm_tile_n(int tile_n);
  * Process-wide; set it between calls. */
 dit_status dit_debug_attention_split(int mode);
 
+/* The bf16 attention runs one of two kernel shapes per call: 8 waves per
+ * workgroup (256 query rows, one workgroup per compute unit) or 4 waves (128
+ * query rows, two workgroups per compute unit).  Key ranges up to 1024 take
+ * the 4-wave shape; so does a single request whose 8-wave items would end in
+ * a split last round when the call holds at most 3 x 64 key tiles of
+ * 256-query items per compute unit.  For tests and tuning: waves = 4 or 8
+ * forces that shape (and the split setting above then applies to the 8-wave
+ * shape only), 0 restores the choice per call; other values give
+ * DIT_ERR_INVALID_ARG.  Without a split both shapes give the same bits.
+ * Process-wide; set it between calls. */
+dit_status dit_debug_attention_shape(int waves);
+
+/* The shape (*waves: 4 or 8) and last-round split (*split_pieces: 0, 2 or 4
+ * key pieces for each of the last request's last *split_items items) that a
+ * bf16 attention call with these ranges takes on a GPU of `compute_units`
+ * compute units, under the current debug settings.  Host arithmetic only: no
+ * device is used.  cu_q, cu_k: host arrays of n_req + 1 offsets from 0, as
+ * for dit_attention_varlen; the outputs are host ints.  A call under graph
+ * capture runs the same shape without the split. */
+dit_status dit_debug_attention_plan(const int32_t *cu_q, const int32_t *cu_k, int n_req, int n_heads,
+                                    int compute_units, int *waves, int *split_pieces, int *split_items);
+
 /* In place on q and (if not NULL) k, each [rows, n_heads*head_dim] with row
  * stride `row_stride`: per-head RMSNorm with gains g_q / g_k (skipped when the
  * gain is NULL), then, if vl != NULL and the sections are not all 0, the

@@ -156,6 +156,10 @@ def lib() -> ctypes.CDLL:
                                         ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
         "dit_debug_gemm_tile_n": (i32, [i32]),
         "dit_debug_attention_split": (i32, [i32]),
+        "dit_debug_attention_shape": (i32, [i32]),
+        "dit_debug_attention_plan": (i32, [ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), i32, i32, i32,
+                                         ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int),
+                                         ctypes.POINTER(ctypes.c_int)]),
         "dit_status_string": (ctypes.c_char_p, [i32]),
         "dit_last_error": (ctypes.c_char_p, []),
         "dit_abi_version": (i32, []),
@@ -176,7 +180,7 @@ def exported_symbols() -> Sequence[str]:
                         "dit_gated_residual", "dit_text_kv_elems", "dit_text_kv", "dit_denoise_workspace_size",
                         "dit_denoise_step", "dit_patchify", "dit_unpatchify_euler", "dit_simulate",
                         "dit_migration_plan", "dit_migration_execute", "dit_debug_gemm_tile_n",
-                        "dit_debug_attention_split",
+                        "dit_debug_attention_split", "dit_debug_attention_shape", "dit_debug_attention_plan",
                         "dit_status_string",
                         "dit_last_error", "dit_abi_version")]
 
@@ -293,6 +297,22 @@ def debug_gemm_tile_n(tile_n: int):
 def debug_attention_split(mode: int):
     """bf16 self-attention's split of its last round: 2 or 4 forces that many key pieces, 1 never, 0 per shape."""
     _check(lib().dit_debug_attention_split(int(mode)), "dit_debug_attention_split")
+
+
+def debug_attention_shape(waves: int):
+    """bf16 attention's kernel shape: 4 or 8 waves forced, 0 chosen per call."""
+    _check(lib().dit_debug_attention_shape(int(waves)), "dit_debug_attention_shape")
+
+
+def debug_attention_plan(cu_q, cu_k, n_heads: int, compute_units: int):
+    """(waves, split pieces, split items) of a bf16 attention call with these ranges (host only)."""
+    n = len(cu_q) - 1
+    cq = (ctypes.c_int32 * (n + 1))(*[int(x) for x in cu_q])
+    ck = (ctypes.c_int32 * (n + 1))(*[int(x) for x in cu_k])
+    w, sp, si = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib().dit_debug_attention_plan(cq, ck, n, int(n_heads), int(compute_units), ctypes.byref(w),
+                                          ctypes.byref(sp), ctypes.byref(si)), "dit_debug_attention_plan")
+    return w.value, sp.value, si.value
 
 
 def timestep_modulation(cfg, weights, t, mod, ws, stream=None):

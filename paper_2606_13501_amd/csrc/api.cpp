@@ -772,6 +772,31 @@ dit_status dit_debug_attention_split(int mode) {
   return DIT_OK;
 }
 
+dit_status dit_debug_attention_shape(int waves) {
+  g_last_error.clear();
+  if (waves != 0 && waves != 4 && waves != 8)
+    return fail(DIT_ERR_INVALID_ARG, "attention shape of %d waves (0, 4 or 8)", waves);
+  set_attention_shape(waves);
+  return DIT_OK;
+}
+
+dit_status dit_debug_attention_plan(const int32_t* cu_q, const int32_t* cu_k, int n_req, int n_heads,
+                                    int compute_units, int* waves, int* split_pieces, int* split_items) {
+  g_last_error.clear();
+  DIT_TRY(check_cu(cu_q, n_req, "cu_q"));
+  DIT_TRY(check_cu(cu_k, n_req, "cu_k"));
+  if (n_heads < 1) return fail(DIT_ERR_INVALID_ARG, "n_heads = %d", n_heads);
+  if (compute_units < 1 || compute_units > 65536)
+    return fail(DIT_ERR_INVALID_ARG, "compute_units = %d outside 1..65536", compute_units);
+  if (!waves || !split_pieces || !split_items) return fail(DIT_ERR_INVALID_ARG, "an output pointer is NULL");
+  DIT_TRY(check_attn_items(cu_q, n_req, n_heads));
+  const AttnPlan pl = attention_plan(cu_q, cu_k, n_req, n_heads, compute_units);
+  *waves = pl.waves;
+  *split_pieces = pl.split_pieces;
+  *split_items = pl.split_items;
+  return DIT_OK;
+}
+
 dit_status dit_timestep_modulation_noalloc(const dit_block_config* cfg, const dit_block_weights* w, int n_req,
                                            const float* t, float* mod, hipStream_t stream) {
   g_last_error.clear();

@@ -641,6 +641,7 @@ static __device__ __align__(256) float attn_part[kMaxPieces * (256 * D + 2 * 256
 namespace {
 
 std::atomic<int> g_split_mode{0};   // 0 per shape, 1 never, 2 or 4 forced
+std::atomic<int> g_shape_mode{0};   // 0 per shape, 4 or 8 waves forced
 
 struct SplitState {
   std::mutex mu;               // a call's enqueue from the event wait to the event record
@@ -679,24 +680,50 @@ struct Split {
   int n = 0;   // split items: the last request's last n
 };
 
-// A launch runs its items in rounds of one workgroup per compute unit.  When
-// the last round is at most half full (a single request; at 720p 11,840 items
-// on 256 CUs leave 64 for a 47th round), those items are split into 2 or 4
-// key pieces, so the last round is 1/2 or 1/4 as long.  Not under graph
-// capture (the split serialises calls through an event recorded outside it).
-Split choose_split(const AttnWork& w, hipStream_t s) {
-  Split sp;
-  const int mode = g_split_mode.load(std::memory_order_relaxed);
-  if (mode == 1 || w.n_req < 1) return sp;
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
-    (void)hipGetLastError();
-    return sp;
+// Work items of query tiles of bq rows: the requests with queries, longest
+// key range first (their tiles do the most work).  Returns the largest key
+// range.
+int build_work(const int* cu_q, const int* cu_k, int n_req, int n_heads, int bq, AttnWork& w) {
+  int order[DIT_MAX_REQ];
+  int n = 0, max_k = 0;
+  for (int r = 0; r < n_req; ++r)
+    if (cu_q[r + 1] > cu_q[r]) {
+      order[n++] = r;
+      max_k = max(max_k, cu_k[r + 1] - cu_k[r]);
+    }
+  for (int i = 1; i < n; ++i) {
+    int x = order[i], j = i - 1;
+    int lx = cu_k[x + 1] - cu_k[x];
+    while (j >= 0 && (cu_k[order[j] + 1] - cu_k[order[j]]) < lx) { order[j + 1] = order[j]; --j; }
+    order[j + 1] = x;
   }
+  w = AttnWork{};
+  w.n_req = n;
+  w.prefix[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    int r = order[i];
+    w.q_start[i] = cu_q[r];
+    w.q_len[i] = cu_q[r + 1] - cu_q[r];
+    w.k_start[i] = cu_k[r];
+    w.k_len[i] = cu_k[r + 1] - cu_k[r];
+    w.tiles_q[i] = (w.q_len[i] + bq - 1) / bq;
+    w.prefix[i + 1] = w.prefix[i] + w.tiles_q[i] * n_heads;
+  }
+  return max_k;
+}
+
+// A launch of the 8-wave shape runs its items in rounds of one workgroup per
+// compute unit.  When the last round is at most half full (a single request;
+// at 720p 11,840 items on 256 CUs leave 64 for a 47th round), those items are
+// split into 2 or 4 key pieces, so the last round is 1/2 or 1/4 as long.
+// Counts only; the launcher drops the split under graph capture (the split
+// serialises calls through an event recorded outside it).
+Split plan_split(const AttnWork& w, int slots, int mode) {
+  Split sp;
+  if (mode == 1 || w.n_req < 1) return sp;
   const int n = w.n_req, last = n - 1;
   const int items = w.prefix[n], items_last = w.prefix[n] - w.prefix[last];
   const int kt_last = (w.k_len[last] + BKV - 1) / BKV;
-  const int slots = cu_count();
   if (mode == 2 || mode == 4) {
     sp.s = mode;
     sp.n = min(items_last, slots / mode);
@@ -708,15 +735,61 @@ Split choose_split(const AttnWork& w, hipStream_t s) {
       sp.n = left;
     }
   }
-  if (sp.s == 0 || sp.n < 1 || sp.n > items_last || kt_last < 8 * sp.s || sp.n * sp.s > kMaxPieces ||
-      !split_state())
+  if (sp.s == 0 || sp.n < 1 || sp.n > items_last || kt_last < 8 * sp.s || sp.n * sp.s > kMaxPieces)
     return Split{};
   return sp;
 }
 
+// Longest launch (in 64-key tiles of 256-query items, per compute unit) that
+// takes the 4-wave shape instead of a split last round.
+constexpr int kSmallLaunchTiles = 3 * 64;
+
+// The shape and split of a bf16 attention launch on `slots` compute units.
+// Key ranges up to kShortKeys take the 4-wave shape.  So does a single request
+// whose 8-wave items would end in a split last round, when the launch is
+// short (at most kSmallLaunchTiles key tiles per compute unit): there the
+// pieces' fixed costs and their merge outweigh the 4-wave shape's 2-3% slower
+// key tiles.  Measured (self-attention, 8-wave with its split against 4-wave):
+// 4,096 tokens x 24 heads 198 against 177 us, 2,048 x 40 106 against 88 us,
+// 4,096 x 40 309 against 289 us; but 6,144 x 24 (96-tile items) 397 against
+// 405 us, and with a full last round the 8-wave shape is 2-3% faster.
+AttnPlan plan_attention(const int* cu_q, const int* cu_k, int n_req, int n_heads, int slots, int split_mode,
+                        int shape_mode, AttnWork& w) {
+  AttnPlan pl;
+  const int max_k = build_work(cu_q, cu_k, n_req, n_heads, 256, w);
+  bool four = max_k <= kShortKeys;
+  if (shape_mode == 4 || shape_mode == 8) {
+    four = shape_mode == 4;
+  } else if (!four && split_mode == 0 && slots > 0 && plan_split(w, slots, 0).s > 0) {
+    int64_t tiles = 0;
+    for (int i = 0; i < w.n_req; ++i)
+      tiles += (int64_t)(w.prefix[i + 1] - w.prefix[i]) * ((w.k_len[i] + BKV - 1) / BKV);
+    four = tiles <= (int64_t)kSmallLaunchTiles * slots;
+  }
+  if (four) {
+    build_work(cu_q, cu_k, n_req, n_heads, 128, w);
+    pl.waves = 4;
+    return pl;
+  }
+  pl.waves = 8;
+  if (slots > 0) {
+    const Split sp = plan_split(w, slots, split_mode);
+    pl.split_pieces = sp.s;
+    pl.split_items = sp.n;
+  }
+  return pl;
+}
+
 }  // namespace
 
+AttnPlan attention_plan(const int* cu_q, const int* cu_k, int n_req, int n_heads, int slots) {
+  AttnWork w;
+  return plan_attention(cu_q, cu_k, n_req, n_heads, slots, g_split_mode.load(std::memory_order_relaxed),
+                        g_shape_mode.load(std::memory_order_relaxed), w);
+}
+
 void set_attention_split(int mode) { g_split_mode.store(mode, std::memory_order_relaxed); }
+void set_attention_shape(int waves) { g_shape_mode.store(waves, std::memory_order_relaxed); }
 
 hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
   const int n_req = p.cq.n_req;
@@ -734,34 +807,12 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
           p.v_stride, p.o_stride, p.n_heads, p.scale, p.cq, p.ck, n_q);
     return hipGetLastError();
   }
-  // requests with queries, longest key range first (their tiles do the most work)
-  int order[DIT_MAX_REQ];
-  int n = 0, max_k = 0;
-  for (int r = 0; r < n_req; ++r)
-    if (p.cq.cu[r + 1] > p.cq.cu[r]) {
-      order[n++] = r;
-      max_k = max(max_k, p.ck.cu[r + 1] - p.ck.cu[r]);
-    }
-  for (int i = 1; i < n; ++i) {
-    int x = order[i], j = i - 1;
-    int lx = p.ck.cu[x + 1] - p.ck.cu[x];
-    while (j >= 0 && (p.ck.cu[order[j] + 1] - p.ck.cu[order[j]]) < lx) { order[j + 1] = order[j]; --j; }
-    order[j + 1] = x;
-  }
-  const bool short_keys = max_k <= kShortKeys;
-  const int bq = short_keys ? 128 : 256;
-  AttnWork w{};
-  w.n_req = n;
-  w.prefix[0] = 0;
-  for (int i = 0; i < n; ++i) {
-    int r = order[i];
-    w.q_start[i] = p.cq.cu[r];
-    w.q_len[i] = p.cq.cu[r + 1] - p.cq.cu[r];
-    w.k_start[i] = p.ck.cu[r];
-    w.k_len[i] = p.ck.cu[r + 1] - p.ck.cu[r];
-    w.tiles_q[i] = (w.q_len[i] + bq - 1) / bq;
-    w.prefix[i + 1] = w.prefix[i] + w.tiles_q[i] * p.n_heads;
-  }
+  AttnWork w;
+  const AttnPlan pl = plan_attention(p.cq.cu, p.ck.cu, n_req, p.n_heads, cu_count(),
+                                     g_split_mode.load(std::memory_order_relaxed),
+                                     g_shape_mode.load(std::memory_order_relaxed), w);
+  const bool short_keys = pl.waves == 4;
+  const int n = w.n_req;
   const int items = w.prefix[n];
   if (items == 0) return hipSuccess;
   if (items > (1 << 27)) return hipErrorInvalidValue;   // keeps (xcd + 1) * n_r in range
@@ -793,7 +844,16 @@ hipError_t launch_attention(const AttnArgs& p, hipStream_t s) {
       else attn_fwd_bf16<8, 4, false><<<grid, 512, 0, s>>>(DIT_ATTN_ARGS);
     }
   };
-  const Split sp = short_keys ? Split{} : choose_split(w, s);
+  Split sp;
+  sp.s = pl.split_pieces;
+  sp.n = pl.split_items;
+  if (sp.s > 0) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone || !split_state()) {
+      (void)hipGetLastError();
+      sp = Split{};
+    }
+  }
   if (sp.s == 0) {
     launch(w, grid_of(w));
     return hipGetLastError();

@@ -49,6 +49,17 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs& p, hipStream_t s);
 // bf16 self-attention's split of its last round (0 per shape, 1 never, 2 or 4 forced).
 void set_attention_split(int mode);
+// bf16 attention's shape (0 per launch, 4 or 8 waves forced).
+void set_attention_shape(int waves);
+// The shape a bf16 attention launch takes on `slots` compute units under the
+// current settings, and the split of its last round (pieces per item and
+// split items; 0 if none).  Host arithmetic only.
+struct AttnPlan {
+  int waves = 8;
+  int split_pieces = 0;
+  int split_items = 0;
+};
+AttnPlan attention_plan(const int* cu_q, const int* cu_k, int n_req, int n_heads, int slots);
 
 // out = LN(x) * mul + add, mul/add per request (modulate: mul = 1 + scale) or
 // shared (affine: gamma, beta).

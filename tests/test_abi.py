@@ -148,6 +148,79 @@ def test_attention_split_hook():
         assert L.dit_debug_attention_split(good) == B.DIT_OK
 
 
+def test_attention_shape_hook():
+    L = _lib()
+    for bad in (1, 2, 16, -4):
+        assert L.dit_debug_attention_shape(bad) == B.DIT_ERR_INVALID_ARG
+        assert b"waves" in L.dit_last_error()
+    for good in (4, 8, 0):   # ends on 0: the choice per call
+        assert L.dit_debug_attention_shape(good) == B.DIT_OK
+
+
+def _cum(lens):
+    out = [0]
+    for n in lens:
+        out.append(out[-1] + n)
+    return out
+
+
+def test_attention_plan_per_launch():
+    """The bf16 attention's shape and split per launch on 256 compute units
+    (host arithmetic).  Self-attention of one request: the 4-wave shape where
+    the 8-wave items would end in a split last round and the launch is short
+    (each such choice measured faster), else the 8-wave shape, split when
+    its last round is at most half full."""
+    plan = B.debug_attention_plan
+    cases = {   # (tokens, heads): (waves, pieces, split items)
+        (1024, 24): (4, 0, 0),       # at most 1024 keys
+        (2048, 24): (8, 0, 0),       # 192 items: one round
+        (3072, 24): (4, 0, 0),       # 288 items, 48-tile items
+        (4096, 24): (4, 0, 0),       # 384 items: a half round left (the image block)
+        (5120, 24): (8, 0, 0),       # 480 items: the last round 7/8 full
+        (6144, 24): (8, 4, 64),      # 576 items of 96 tiles: too long for 4 waves
+        (2048, 40): (4, 0, 0),
+        (4096, 40): (4, 0, 0),       # 640 items of 64 tiles: 160 tiles per CU
+        (8192, 40): (8, 0, 0),       # 5 full rounds
+        (75600, 40): (8, 4, 64),     # 720p: 11,840 items, 64 left for a 47th round
+    }
+    for (T, H), want in cases.items():
+        assert plan(_cum([T]), _cum([T]), H, 256) == want, (T, H)
+    assert plan(_cum([75600]), _cum([512]), 40, 256) == (4, 0, 0)               # cross-attention
+    assert plan(_cum([512, 1152, 4095, 9450]), _cum([4096, 9216, 32760, 75600]), 40, 256) == (8, 0, 0)
+    # the same launch on 200 compute units: 384 items leave 184 for a second
+    # round, more than half of it, so nothing is split and 8 waves run it
+    assert plan(_cum([4096]), _cum([4096]), 24, 200) == (8, 0, 0)
+    try:
+        B.debug_attention_split(2)
+        assert plan(_cum([4096]), _cum([4096]), 24, 256) == (8, 2, 128)         # forced split: 8 waves
+        B.debug_attention_split(1)
+        assert plan(_cum([75600]), _cum([75600]), 40, 256) == (8, 0, 0)
+        B.debug_attention_split(0)
+        B.debug_attention_shape(4)
+        assert plan(_cum([75600]), _cum([75600]), 40, 256) == (4, 0, 0)
+        B.debug_attention_shape(8)
+        assert plan(_cum([4096]), _cum([4096]), 24, 256) == (8, 2, 128)
+        assert plan(_cum([100]), _cum([77]), 2, 256) == (8, 0, 0)
+    finally:
+        B.debug_attention_split(0)
+        B.debug_attention_shape(0)
+
+
+def test_attention_plan_rejects_bad_arguments():
+    L = _lib()
+    cu = (ctypes.c_int32 * 2)(0, 100)
+    bad_cu = (ctypes.c_int32 * 2)(5, 100)
+    out = [ctypes.c_int() for _ in range(3)]
+    refs = [ctypes.byref(x) for x in out]
+    assert L.dit_debug_attention_plan(cu, cu, 1, 2, 256, *refs) == B.DIT_OK
+    assert L.dit_debug_attention_plan(bad_cu, cu, 1, 2, 256, *refs) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_debug_attention_plan(cu, cu, 0, 2, 256, *refs) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_debug_attention_plan(cu, cu, 1, 0, 256, *refs) == B.DIT_ERR_INVALID_ARG
+    assert L.dit_debug_attention_plan(cu, cu, 1, 2, 0, *refs) == B.DIT_ERR_INVALID_ARG
+    assert b"compute_units" in L.dit_last_error()
+    assert L.dit_debug_attention_plan(cu, cu, 1, 2, 256, None, refs[1], refs[2]) == B.DIT_ERR_INVALID_ARG
+
+
 def test_norm_kernels_reject_bad_arguments():
     L = _lib()
     S = ctypes.c_void_p(0)

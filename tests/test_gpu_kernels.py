@@ -294,6 +294,85 @@ def test_attention_split_into_key_pieces(H, lq, lk, pieces):
     check(host(out2), ref2, "bf16", f"attention split into {pieces}, second call")
 
 
+class forced_attention_shape:
+    """Force the bf16 attention's kernel shape (4 or 8 waves) and its split
+    setting inside a with-block; the choices per call again afterwards."""
+
+    def __init__(self, B, waves, split=0):
+        self.B, self.waves, self.split = B, waves, split
+
+    def __enter__(self):
+        self.B.debug_attention_shape(self.waves)
+        self.B.debug_attention_split(self.split)
+
+    def __exit__(self, *exc):
+        self.B.debug_attention_shape(0)
+        self.B.debug_attention_split(0)
+
+
+SHAPE_CASES = [
+    # heads, query lengths, key lengths (None = self-attention), all over 1024 keys
+    (2, [3000], None),                     # 47 key tiles, the last of 56 keys
+    (2, [2600, 2100, 70], None),           # packed, ragged in queries and keys
+    (1, [300, 200], [4000, 2100]),         # cross-shaped ranges
+]
+
+
+@pytest.mark.parametrize("H,lq,lk", SHAPE_CASES)
+def test_attention_four_wave_shape_on_long_ranges(H, lq, lk):
+    """The 4-wave shape (128 query rows per workgroup) forced on key ranges
+    over 1024 equals the oracle, and the 8-wave shape without a split gives
+    the same bits."""
+    B = require_gpu()
+    d = 128
+    cu_q = _cu(lq)
+    cu_k = cu_q if lk is None else _cu(lk)
+    Tq, Tk, W = int(cu_q[-1]), int(cu_k[-1]), H * d
+    qb = synth.draw((Tq, W), (37, H, Tq, Tk), "bf16")
+    kvb = synth.draw((Tk, 2 * W), (38, H, Tq, Tk), "bf16")
+    ref = O.attention_varlen(O.decode(qb), O.decode(kvb)[:, :W], O.decode(kvb)[:, W:], cu_q, cu_k, H, d)
+    log(f"case attention 4-wave shape H={H} lq={lq} lk={lk}")
+    qt, kvt = dev(qb), dev(kvb)
+    out4, out8 = empty((Tq, W), "bf16"), empty((Tq, W), "bf16")
+    with forced_attention_shape(B, 4):
+        B.attention_varlen(qt, kvt[:, :W], kvt[:, W:], out4, cu_q, cu_k, H, d)
+        torch.cuda.synchronize()
+    with forced_attention_shape(B, 8, split=1):
+        B.attention_varlen(qt, kvt[:, :W], kvt[:, W:], out8, cu_q, cu_k, H, d)
+        torch.cuda.synchronize()
+    check(host(out4), ref, "bf16", "attention, 4-wave shape")
+    assert torch.equal(out4, out8), "the two shapes differ"
+
+
+def test_attention_short_launch_takes_four_waves():
+    """One request of 4,000 tokens x 24 heads (the image block's shape, ragged
+    keys): its 8-wave items would end in a split last round, and the launch
+    is short, so on 256 compute units it runs the 4-wave shape.  The first
+    and last row of every 128-row query tile and the last rows equal the
+    oracle, and the output equals the 8-wave shape's without a split."""
+    B = require_gpu()
+    H, d, T = 24, 128, 4000
+    W = H * d
+    cu = _cu([T])
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    waves = B.debug_attention_plan(cu, cu, H, cus)[0]
+    log(f"case attention short launch H={H} T={T} on {cus} CUs: {waves} waves")
+    if waves != 4:
+        pytest.skip(f"{cus} compute units: the launch does not take the 4-wave shape")
+    qkv = synth.draw((T, 3 * W), (39, H, T), "bf16")
+    t = dev(qkv)
+    out, out8 = empty((T, W), "bf16"), empty((T, W), "bf16")
+    B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], out, cu, cu, H, d)
+    with forced_attention_shape(B, 8, split=1):
+        B.attention_varlen(t[:, :W], t[:, W:2 * W], t[:, 2 * W:], out8, cu, cu, H, d)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(0, T, 128), np.arange(127, T, 128), np.arange(T - 8, T)]))
+    src = O.decode(qkv)
+    ref = O.attention_varlen(src[:, :W], src[:, W:2 * W], src[:, 2 * W:], cu, cu, H, d, q_rows=rows)
+    check(host(out)[rows], ref, "bf16", "attention, short launch")
+    assert torch.equal(out, out8), "the two shapes differ"
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
 def test_attention_request_without_keys(dtype, d):
     """A request with queries but no keys gets rows of zeros; the packed
