@@ -37,6 +37,8 @@ constexpr int kStageBytes = 2 * kTileBytes;         // A tile + W tile
 constexpr int kLoads = kTileBytes / 1024 / kWaves;  // 1 KiB loads per wave, operand and step (8)
 constexpr int kEpiBytes = 32 * 256;                 // per wave: 32 rows x 64 fp32 (epilogue window)
 constexpr int kGroupM = 2;                          // tile rows per raster group
+constexpr int kGroupMFew = 8;                       // the same, at most kFewTileRows tile rows
+constexpr int kFewTileRows = 16;
 constexpr int kXcds = 8;                            // gfx950: 8 XCDs, workgroups dispatched round-robin
 
 // gelu_tanh(z) = z (1 + tanh u) / 2 = z / (1 + e^(-2u)), u = sqrt(2/pi) (z + 0.044715 z^3)
@@ -51,27 +53,32 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 // Tile sequence of a workgroup.  Each XCD owns a contiguous range of logical
 // tiles (the dispatcher places workgroup b on XCD b mod 8); the workgroups of
 // one XCD take its tiles round-robin, so at any time they work on adjacent
-// tiles.  Logical tiles are rastered in groups of kGroupM tile rows, so the
+// tiles.  Logical tiles are rastered in groups of group_m tile rows, so the
 // tiles resident on one XCD share A and W panels in its L2.  Two tile rows per
-// group measured best (1-2.5% over 4, 8 and 16 at 75,600 x 5,120): the weights
+// group measured best at 75,600 rows (1-2.5% over 4, 8 and 16): the weights
 // of one GEMM (at most 157 MB) stay in the 256 MB MALL, so reuse of the
-// activation rows is what saves memory traffic.
+// activation rows is what saves memory traffic.  With at most 16 tile rows
+// (4,096 rows: one to three rounds of tiles), groups of 8 rows: an XCD's 32
+// resident tiles then cover 8 x 4 tiles instead of 2 x 16 and read a quarter
+// of the W columns per step.  Measured in alternating order on one box at
+// 4,096 rows: 0.2-0.8% faster with D = 3,072 (output, up and down
+// projections), the same on the QKV shape.
 struct TileSeq {
   int first, stride, count;   // logical tiles first + stride * it, it < count
-  int tiles_m, tiles_n;
+  int tiles_m, tiles_n, group_m;
   __device__ void coords(int it, int& tm, int& tn) const {
     const int t = first + stride * it;
-    const int width = kGroupM * tiles_n;
+    const int width = group_m * tiles_n;
     const int group = t / width;
-    const int first_m = group * kGroupM;
-    const int gsize = min(tiles_m - first_m, kGroupM);
+    const int first_m = group * group_m;
+    const int gsize = min(tiles_m - first_m, group_m);
     const int r = t - group * width;
     tm = first_m + r % gsize;
     tn = r / gsize;
   }
 };
 
-__device__ __forceinline__ TileSeq tile_seq(int b, int nb, int tiles_m, int tiles_n) {
+__device__ __forceinline__ TileSeq tile_seq(int b, int nb, int tiles_m, int tiles_n, int group_m) {
   const int tiles = tiles_m * tiles_n;
   const int per_xcd = (tiles + kXcds - 1) / kXcds;
   const int x = b % kXcds, slot = b / kXcds, wgs = nb / kXcds;
@@ -82,6 +89,7 @@ __device__ __forceinline__ TileSeq tile_seq(int b, int nb, int tiles_m, int tile
   q.count = q.first < hi ? (hi - q.first + wgs - 1) / wgs : 0;
   q.tiles_m = tiles_m;
   q.tiles_n = tiles_n;
+  q.group_m = group_m;
   return q;
 }
 
@@ -125,7 +133,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
     const bf16* __restrict__ A, int64_t lda, const bf16* __restrict__ W, int64_t ldw,
     const bf16* __restrict__ bias, bf16* __restrict__ C, int64_t ldc, const bf16* R, int64_t ldr,
     const float* __restrict__ gate, int64_t gate_stride, ReqTable req, int M, int N, int K,
-    int tiles_m, int tiles_n, int plane_cols, int64_t plane_skip) {
+    int tiles_m, int tiles_n, int group_m, int plane_cols, int64_t plane_skip) {
   constexpr int WN = BNT / 2;                    // columns of a wave's sub-tile
   constexpr int NI = WN / 32;                    // its W blocks of 32 columns (4 or 3)
   constexpr int kTileW = BNT * kRowBytes;        // the W tile of one step
@@ -133,7 +141,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_nt(
   constexpr int kLW = kTileW / 1024 / kWaves;    // 1 KiB W loads per wave and step (8 or 6)
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStage + kWaves * kEpiBytes];
 
-  const TileSeq seq = tile_seq(blockIdx.x, gridDim.x, tiles_m, tiles_n);
+  const TileSeq seq = tile_seq(blockIdx.x, gridDim.x, tiles_m, tiles_n, group_m);
   if (seq.count == 0) return;
   int tm, tn;
   seq.coords(0, tm, tn);
@@ -592,6 +600,7 @@ hipError_t launch_bf16_tiles(const LinearArgs& p, int tiles_m, int tiles_n, hipS
   const int tiles = tiles_m * tiles_n;
   int grid = (tiles + kXcds - 1) / kXcds * kXcds;   // one tile per workgroup
   const int kt = p.K / BK;
+  const int group_m = tiles_m <= kFewTileRows ? kGroupMFew : kGroupM;
   if (kt % 2 == 0 && kt >= 6) {
     // one workgroup per compute unit, each running a sequence of tiles
     const int resident = cu_count() / kXcds * kXcds;
@@ -599,12 +608,12 @@ hipError_t launch_bf16_tiles(const LinearArgs& p, int tiles_m, int tiles_n, hipS
     gemm_bf16_nt<EPI, true, BNT><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
         (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
-        p.plane_cols, p.plane_stride - p.plane_cols);
+        group_m, p.plane_cols, p.plane_stride - p.plane_cols);
   } else {
     gemm_bf16_nt<EPI, false, BNT><<<grid, kThreads, 0, s>>>(
         (const bf16*)p.a, p.lda, (const bf16*)p.w, p.ldw, (const bf16*)p.bias, (bf16*)p.out, p.ldo,
         (const bf16*)p.res, p.ldr, p.gate, p.gate_stride, p.req, (int)p.M, p.N, p.K, tiles_m, tiles_n,
-        p.plane_cols, p.plane_stride - p.plane_cols);
+        group_m, p.plane_cols, p.plane_stride - p.plane_cols);
   }
   return hipGetLastError();
 }

@@ -64,6 +64,10 @@ GEMM_CASES = [
     ("bf16", 1000, 768, 1024, [1000]),       # ragged M, several tiles
     ("bf16", 300, 264, 64, [100, 200]),       # N tail (not a multiple of 256), K = one tile
     ("bf16", 4096 + 77, 512, 3072, [4096, 77]),
+    # 11 and 16 tile rows: rastered in groups of 8 tile rows (a full group and
+    # a tail of 3; more tiles than compute units, so tile sequences)
+    ("bf16", 2600, 1024, 384, [2600]),
+    ("bf16", 3900, 5120 + 64, 384, [1900, 2000]),
     ("f32", 64, 1536, 384, [64]),
     ("f32", 77, 768, 384, [30, 47]),
 ]
