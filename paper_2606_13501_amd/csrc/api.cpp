@@ -401,10 +401,13 @@ SideStream* side_stream() {
 
 // S5..S12 on this GPU's rows given the self-attention output o.
 // With kv != NULL the text keys and values come from that cache ([txt_rows, 2D],
-// normalised keys) and txt is not read.
+// normalised keys) and txt is not read; kv_side != NULL: kv is still being
+// written on that side stream, whose join event s waits for before the
+// cross-attention (the caller holds its mutex).
 dit_status post_attention_impl(const dit_block_config* c, const dit_block_weights* w, const dit_varlen* vl,
                                const void* x, const void* o, const void* txt, const float* mod, void* y,
-                               const Workspace& ws, hipStream_t s, const void* kv = nullptr) {
+                               const Workspace& ws, hipStream_t s, const void* kv = nullptr,
+                               SideStream* kv_side = nullptr) {
   const int D = c->hidden, Dff = c->mlp_hidden;
   const int64_t T = vl->cu_seqlens[vl->n_req];
   const int64_t L = vl->cu_seqlens_txt[vl->n_req];
@@ -414,7 +417,7 @@ dit_status post_attention_impl(const dit_block_config* c, const dit_block_weight
   const dit_dtype dt = c->dtype;
   // [ck | cv] = txt W_ckv^T + b_ckv ; ck = RMS(ck), on the side stream when there is one
   const char* ckv = (const char*)kv;
-  SideStream* side = nullptr;
+  SideStream* side = kv ? kv_side : nullptr;
   std::unique_lock<std::mutex> side_lock;
   if (!ckv) {
     side = side_stream();
@@ -697,6 +700,19 @@ dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weight
   DIT_TRY(check_ptr(y, "y"));
   Workspace W;
   DIT_TRY(check_ws(cfg, vl, ws, ws_bytes, &W));
+  // The text keys and values depend on txt and the weights only: on the side
+  // stream from the start, beside the conditioning, LayerNorm and QKV
+  // projection, joined before the cross-attention.
+  SideStream* side = side_stream();
+  std::unique_lock<std::mutex> side_lock;
+  if (side) {
+    const int64_t L = vl->cu_seqlens_txt[vl->n_req];
+    side_lock = std::unique_lock<std::mutex>(side->mu);
+    DIT_HIP(hipEventRecord(side->fork, stream), "hipEventRecord");
+    DIT_HIP(hipStreamWaitEvent(side->stream, side->fork, 0), "hipStreamWaitEvent");
+    DIT_TRY(text_kv_impl(cfg, w, L, make_req(vl->cu_seqlens_txt, vl->n_req), txt, W.ckv, side->stream));
+    DIT_HIP(hipEventRecord(side->join, side->stream), "hipEventRecord");
+  }
   const float* m = mod;
   if (!m) {
     DIT_TRY(run_cond(cfg, w, vl->n_req, t, W.mod, W.e, W.a1, W.c, stream));
@@ -704,7 +720,7 @@ dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weight
   }
   DIT_TRY(pre_attention_impl(cfg, w, vl, x, m, W.qkv, W, stream));
   DIT_TRY(self_attention_impl(cfg, vl, W.qkv, W.o, stream));
-  return post_attention_impl(cfg, w, vl, x, W.o, txt, m, y, W, stream);
+  return post_attention_impl(cfg, w, vl, x, W.o, txt, m, y, W, stream, side ? W.ckv : nullptr, side);
 }
 
 dit_status dit_block_pre_attention(const dit_block_config* cfg, const dit_block_weights* w, const dit_varlen* vl,
