@@ -519,36 +519,7 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void attn_fwd_bf16(
     return;
   }
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;   // no keys: output 0
-  if constexpr (RING == 2) {
-    // The 4-wave shape's items are a few key tiles long, so the store of O
-    // is a large share of them.  In the MFMA layout a lane holds 16 bytes of
-    // one row per d block, and a store instruction would touch 32 rows; so
-    // each wave writes its 32 x 128 block into a private 8 KiB of LDS and
-    // reads it back as whole rows (4 rows of 256 bytes per instruction).  The
-    // space is the ring slot of tile n_tiles - 2 (slot n_tiles % 2): every
-    // wave finished with that tile before the barrier that ended its step,
-    // nothing is issued into it afterwards, and with n_tiles < 2 nothing ever
-    // was.  16-byte chunks are XOR-swizzled by row % 16, so neither the
-    // writes nor the reads meet in one bank.
-    char* stage = smem + (n_tiles % 2) * kSlotBytes + wave * 8192;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16x4 ov;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) ov[jj] = (bf16)(oacc[db][4 * i + jj] * inv);
-        *reinterpret_cast<bf16x4*>(stage + fr * 256 + (((4 * db + i) ^ (fr & 15)) << 4) + 8 * fh) = ov;
-      }
-    const int c = lane & 15;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int r = 4 * u + (lane >> 4);
-      const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * 256 + ((c ^ (r & 15)) << 4));
-      const int row = q0 + 32 * wave + r;
-      if (row < q_end) *reinterpret_cast<bf16x8*>(O + (int64_t)row * os + head * D + 8 * c) = v;
-    }
-  } else if (my_q < q_end) {
+  if (my_q < q_end) {
     bf16* op = O + (int64_t)my_q * os + head * D + 4 * fh;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
