@@ -183,3 +183,38 @@ def test_scanner_flags_a_copy_before_the_wait_states():
     short = [";;#ASMSTART", "v_mfma_f32_32x32x16_bf16 v[96:111], v[1:4], v[5:8], v[96:111]", "s_nop 7",
              ";;#ASMEND", "v_exp_f32_e32 v10, v96"]
     assert len(scan(short)) >= 1
+
+
+def _steady_loop(body):
+    """The first loop (a backward branch) of a kernel holding exactly the 32
+    MFMAs of one key tile: the steady key-tile loop."""
+    labels = {}
+    for i, l in enumerate(body):
+        m = re.match(r"^(\.LBB\w+):", l)
+        if m:
+            labels[m.group(1)] = i
+    for i, l in enumerate(body):
+        m = re.match(r"\s+s_(cbranch_\w+|branch)\s+(\.LBB\w+)", l)
+        if m and labels.get(m.group(2), i) < i:
+            ins = [x.strip().split()[0] for x in body[labels[m.group(2)]:i + 1]
+                   if x.strip() and not x.strip().startswith((".", ";")) and not x.strip().endswith(":")]
+            if sum(1 for x in ins if x.startswith("v_mfma")) == 32:
+                return ins
+    return None
+
+
+# Instructions of the steady key-tile loop as the library's flags compile it
+# (8 waves: 233, 4 waves: 237), plus a small margin.  A change elsewhere in
+# the kernel can make the compiler schedule this loop differently: a staged
+# output store in the epilogue once grew the 4-wave loop to 257 instructions
+# (each PV MFMA waiting for its own fragment reads) and made the 4-wave
+# self-attention 8-12% slower.  A failure here asks for a timing check.
+MAX_LOOP = {"ILi8ELi4E": 240, "ILi4ELi2E": 244}
+
+
+def test_key_tile_loop_stays_compact(attention_asm):
+    for name, body in _kernels(attention_asm):
+        ins = _steady_loop(body)
+        assert ins is not None, f"{name}: no loop of 32 MFMAs"
+        limit = next(v for k, v in MAX_LOOP.items() if k in name)
+        assert len(ins) <= limit, f"{name}: steady loop of {len(ins)} instructions (at most {limit})"
